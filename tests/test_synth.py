@@ -1,0 +1,61 @@
+"""The seeded generator: determinism, shapes, regions and the density band."""
+import numpy as np
+import torch
+
+import oracle
+import synth
+
+
+def test_shapes_and_seq_lengths():
+    expect = {0: (192, 3, 64), 1: (32760, 256, 120), 2: (17776, 139, 112), 3: (75600, 591, 80),
+              4: (119056, 931, 16)}
+    for wid, (n, nb, tail) in expect.items():
+        wl = synth.WORKLOADS[wid]
+        assert (wl.seq_len, wl.n_blocks, wl.tail_valid) == (n, nb, tail)
+
+
+def test_same_seed_same_bits_different_seed_different_bits():
+    wl = synth.WORKLOADS[0]
+    a = synth.attention_inputs(wl, seed=0)
+    b = synth.attention_inputs(wl, seed=0)
+    c = synth.attention_inputs(wl, seed=1)
+    for name in ("q", "k", "v", "q_hist", "k_hist"):
+        assert a[name].dtype == torch.bfloat16 and a[name].shape == (1, 2, 192, 64)
+        assert torch.equal(a[name].view(torch.int16), b[name].view(torch.int16))
+        assert not torch.equal(a[name], c[name])
+
+
+def test_head_subset_matches_full():
+    wl = synth.WORKLOADS[0]
+    full = synth.attention_inputs(wl, seed=3)
+    one = synth.attention_inputs(wl, seed=3, heads=1)
+    assert torch.equal(full["k"][:, :1], one["k"])
+
+
+def test_region_counts_and_text_blocks():
+    for wid in (1, 2, 3, 4):
+        wl = synth.WORKLOADS[wid]
+        rows, cols, info = synth.region_flags(wl, 0)
+        assert info["target_blocks"] >= wl.target_blocks
+        assert info["target_blocks"] <= wl.target_blocks + 8
+        if wl.n_text:
+            text = np.unique(np.arange(wl.n_text) // wl.block)
+            assert cols[0, text].all() and rows[0, text].all()
+            assert cols.sum() == len(text)
+        else:
+            assert cols is None
+
+
+def test_signature_planted_row():
+    s = synth.signature_inputs(m=64, dim=16, nq=2, seed=0)
+    d = s["query"][1] - s["bank"][s["planted"]]
+    assert 0.2 < float(d.std()) < 0.8
+
+
+def test_historical_density_in_band():
+    # The field amplitude is calibrated so that the historical mask of the
+    # 32K-token workload keeps 15-25 % of its blocks at threshold 0.9.
+    wl = synth.WORKLOADS[1]
+    x = synth.attention_inputs(wl, seed=0)
+    m, rep = oracle.build_block_mask(oracle.to_f64(x["q_hist"]), oracle.to_f64(x["k_hist"]), wl.block, wl.tau)
+    assert 0.15 <= m.mean() <= 0.25
