@@ -1,0 +1,206 @@
+"""Benchmark of the whole cache-hit block-sparse attention path on one MI355X.
+
+One step = the four rows of the path on one batch of synthetic input that is
+already resident in HBM:
+  1. historical block mask from pooled Q_hist.K_hist (carnator_build_block_mask)
+  2. target-row widening (carnator_merge_target_rows)
+  3. block-sparse attention of the target Q, K, V (carnator_block_sparse_attn,
+     which also compacts the mask)
+  4. Early-Signature cosine top-k against the 4096 x 3072 bank
+     (carnator_signature_sim)
+Three input sets are rotated so the 256 MB Infinity Cache does not serve
+repeated reads of the HBM-bound steps.
+
+Prints one JSON line.  ``value`` is executed attention TFLOP per step divided
+by the step time (whole-job throughput); ``roofline`` describes the attention
+kernel against the bf16 MFMA peak.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "block-sparse attn ms/call + executed TFLOP/s (% bf16 MFMA peak) at 32K tokens"
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 FLOP/clk x 2.4 GHz (dense)
+PEAK_HBM_GBPS = 8000.0
+
+
+def executed_flops(mask: np.ndarray, N: int, bs: int, d: int) -> float:
+    """sum over kept (b,h,i,j) of 4 d n_i n_j (QK^T and PV, valid tokens only)."""
+    nb = mask.shape[-1]
+    n = np.full(nb, bs, dtype=np.float64)
+    n[-1] = N - (nb - 1) * bs
+    kept = (mask != 0).astype(np.float64)
+    return float(4.0 * d * np.einsum("bhij,i,j->", kept, n, n))
+
+
+def dense_flops(B, H, N, d) -> float:
+    return 4.0 * d * B * H * float(N) * float(N)
+
+
+def cpu_baseline(wl, heads: int = 2):
+    """The oracle, as it stands, on a bounded sample: every step of the path
+    for ``heads`` heads of the workload (mask, widening, attention of all
+    query blocks of those heads) plus the full signature scan."""
+    import oracle
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas = 1
+    x = synth.attention_inputs(wl, seed=0, device="cpu", heads=heads)
+    sig = synth.signature_inputs()
+    t0 = time.perf_counter()
+    m, _ = oracle.build_block_mask(oracle.to_f64(x["q_hist"]), oracle.to_f64(x["k_hist"]), wl.block, wl.tau)
+    cols = None if x["col_flags"] is None else x["col_flags"].numpy()
+    merged = oracle.merge_target_rows(m, x["row_flags"].numpy(), cols)
+    oracle.block_sparse_attention(oracle.to_f64(x["q"]), oracle.to_f64(x["k"]), oracle.to_f64(x["v"]), merged,
+                                  wl.block)
+    oracle.topk_cosine(sig["query"].numpy(), sig["bank"].numpy(), 8)
+    dt = time.perf_counter() - t0
+    fl = executed_flops(merged, wl.seq_len, wl.block, wl.head_dim)
+    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": blas, "kind": "oracle",
+            "host_cpus": len(os.sched_getaffinity(0)), "seconds": dt,
+            "sample": "%d of %d heads of %s, full path (mask, widening, attention of all %d query blocks) "
+                      "+ 1 signature scan" % (heads, wl.heads, wl.name, wl.n_blocks)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=1)
+    ap.add_argument("--sets", type=int, default=3, help="input sets rotated across steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(the attention, mask and scan shard by head / bank rows with no exchange inside "
+              "an operator; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_32420_amd as P
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = synth.WORKLOADS[args.workload]
+    B, H, N, d, bs, nb = wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block, wl.n_blocks
+    print("bench: generating %d input sets of %s" % (args.sets, wl.name), file=sys.stderr, flush=True)
+    sets = []
+    for sidx in range(args.sets):
+        x = synth.attention_inputs(wl, seed=sidx, device=dev)
+        sg = synth.signature_inputs(seed=sidx, device=dev)
+        sets.append((x, sg))
+    stream = torch.cuda.current_stream(dev)
+    # persistent outputs and workspaces: nothing is allocated inside the timed region
+    masks = [torch.empty(B, H, nb, nb, dtype=torch.uint8, device=dev) for _ in sets]
+    outs = [torch.empty(B, H, N, d, dtype=torch.bfloat16, device=dev) for _ in sets]
+    ws_attn = P.block_sparse_attn_workspace(sets[0][0]["q"], bs)
+    ws_mask = P.build_block_mask_workspace(sets[0][0]["q_hist"], bs)
+    ws_sig = P.signature_sim_workspace(synth.SIG_NQ, synth.SIG_M, synth.SIG_TOPK, dev)
+    sig_out = (torch.empty(synth.SIG_NQ, synth.SIG_TOPK, dtype=torch.int32, device=dev),
+               torch.empty(synth.SIG_NQ, synth.SIG_TOPK, dtype=torch.float32, device=dev))
+    flags = [(x["row_flags"].contiguous(), None if x["col_flags"] is None else x["col_flags"].contiguous())
+             for x, _ in sets]
+
+    ev = {k: [] for k in ("build", "merge", "attn", "sig")}
+
+    def step(i, record):
+        si = i % len(sets)
+        x, sg = sets[si]
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(5)] if record else None
+        if record:
+            e[0].record(stream)
+        P.build_block_mask(x["q_hist"], x["k_hist"], bs, wl.tau, out=masks[si], workspace=ws_mask)
+        if record:
+            e[1].record(stream)
+        P.merge_target_rows(masks[si], flags[si][0], flags[si][1])
+        if record:
+            e[2].record(stream)
+        P.block_sparse_attn(x["q"], x["k"], x["v"], masks[si], bs, out=outs[si], workspace=ws_attn)
+        if record:
+            e[3].record(stream)
+        P.signature_sim(sg["query"], sg["bank"], synth.SIG_TOPK, workspace=ws_sig, out=sig_out)
+        if record:
+            e[4].record(stream)
+            ev["build"].append((e[0], e[1]))
+            ev["merge"].append((e[1], e[2]))
+            ev["attn"].append((e[2], e[3]))
+            ev["sig"].append((e[3], e[4]))
+
+    for i in range(args.warmup):
+        step(i, False)
+    torch.cuda.synchronize()
+    print("bench: warmup done, timing %d steps" % args.steps, file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+
+    def avg_ms(name):
+        return float(np.mean([a.elapsed_time(b) for a, b in ev[name]]))
+
+    # algorithmic work of one step (averaged over the rotated sets)
+    fl_exec = float(np.mean([executed_flops(m.cpu().numpy(), N, bs, d) for m in masks]))
+    density = float(np.mean([m.float().mean().item() for m in masks]))
+    fl_dense = dense_flops(B, H, N, d)
+    attn_ms = avg_ms("attn")
+    build_ms = avg_ms("build")
+    sig_ms = avg_ms("sig")
+    builder_bytes = 2.0 * B * H * N * d * 2 + B * H * nb * nb
+    sig_bytes = 4.0 * synth.SIG_M * synth.SIG_D + 4.0 * synth.SIG_NQ * synth.SIG_D + 8.0 * synth.SIG_NQ * synth.SIG_TOPK
+    attn_tflops = fl_exec / (attn_ms * 1e-3) / 1e12
+    res = {
+        "metric": METRIC,
+        "value": round(fl_exec / (ms_step * 1e-3) / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "heads": H, "seq_len": N, "head_dim": d, "block": bs,
+                   "mass_threshold": wl.tau, "mask_density": round(density, 4),
+                   "signature_bank": [synth.SIG_M, synth.SIG_D], "topk": synth.SIG_TOPK,
+                   "input_sets": len(sets), "parallelism": "none (1 GPU)"},
+        "attn_ms_per_call": round(attn_ms, 4),
+        "attn_executed_tflop": round(fl_exec / 1e12, 4),
+        "attn_dense_equiv_tflop": round(fl_dense / 1e12, 4),
+        "attn_executed_tflops": round(attn_tflops, 2),
+        "attn_dense_equiv_tflops": round(fl_dense / (attn_ms * 1e-3) / 1e12, 2),
+        "attn_pct_bf16_peak": round(100.0 * attn_tflops / PEAK_BF16_TFLOPS, 2),
+        "builder_ms_per_call": round(build_ms, 4),
+        "builder_GBps": round(builder_bytes / (build_ms * 1e-3) / 1e9, 1),
+        "builder_pct_hbm_peak": round(100.0 * builder_bytes / (build_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 2),
+        "merge_ms_per_call": round(avg_ms("merge"), 4),
+        "sig_ms_per_call": round(sig_ms, 4),
+        "sig_GBps": round(sig_bytes / (sig_ms * 1e-3) / 1e9, 1),
+        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "kernel": "block_sparse_attn call (compaction + V transpose + attention kernel)"},
+    }
+    if not args.no_cpu_baseline:
+        print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

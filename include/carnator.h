@@ -1,0 +1,219 @@
+/*
+ * carnator.h -- C ABI of the cache-hit block-sparse attention path on MI355X
+ * (gfx950).
+ *
+ * The operations follow the paper "Carnator: Fast Text-to-Video Generation
+ * with Generation-Native Compatibility-Guided Cross-Request Reuse":
+ *
+ *   carnator_build_block_mask   historical block connectivity (Appendix C.3)
+ *   carnator_merge_target_rows  target-specific query blocks widened to full
+ *                               rows (Sec. 3.3, joint reuse in the middle
+ *                               layers)
+ *   carnator_compact_block_mask per-row lists of kept key blocks
+ *   carnator_block_sparse_attn  attention of the recomputed target Q, K, V
+ *                               under the reused structure (Sec. 3.3,
+ *                               historical sparse-connectivity reuse)
+ *   carnator_signature_sim      cosine scoring of an early-step signature
+ *                               against a bank of cached signatures (Sec. 3.1,
+ *                               Sec. 4.1 candidate recall)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers named in the argument lists are DEVICE pointers unless a comment
+ *   says "host".  Descriptor structs (carnator_shape, carnator_view) are read
+ *   on the host during the call and not retained.
+ * - Every call that takes a stream only enqueues work on it and returns; the
+ *   results are ready when the stream is synchronised.  stream may be NULL
+ *   (the default stream).
+ * - Ownership: the caller owns every buffer, the workspace and the stream.
+ *   The library allocates no device memory, keeps no pointer after it returns
+ *   and holds no global mutable state apart from a thread-local error string.
+ *   Calls that run concurrently need separate workspaces.
+ * - Errors: each call returns a carnator_status.  On a non-OK status nothing
+ *   has been enqueued and no output has been written.  All argument checks
+ *   happen before the first HIP call.  A failed launch returns
+ *   CARNATOR_E_HIP; faults inside a kernel surface at the caller's next
+ *   synchronisation.  carnator_last_error() gives a text detail for the
+ *   calling thread.
+ * - Token layout: Q, K, V and O are bf16 [B, H, N, d] with d contiguous and
+ *   arbitrary element strides for B, H and N (stride_n a multiple of 8,
+ *   data 16-byte aligned).  Blocks are runs of `block` consecutive tokens;
+ *   block j covers tokens [j*block, min((j+1)*block, N)), so only the last
+ *   block can be partial.  nB = ceil(N / block).  Tokens past N are never
+ *   read or written.
+ * - Block masks are uint8 [B, H, nB, nB], contiguous; 0 drops a block pair,
+ *   any other byte keeps it.  The builder writes exactly 0 or 1.
+ * - Supported: head_dim in {64, 128}, block in {64, 128}.  Anything else
+ *   returns CARNATOR_E_UNSUPPORTED.
+ */
+#ifndef CARNATOR_H
+#define CARNATOR_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CARNATOR_ABI_VERSION 1
+
+typedef enum {
+  CARNATOR_OK = 0,
+  CARNATOR_E_NULL = -1,        /* a required pointer is NULL */
+  CARNATOR_E_SHAPE = -2,       /* a size or stride is out of range */
+  CARNATOR_E_UNSUPPORTED = -3, /* head_dim / block / topk not supported */
+  CARNATOR_E_ALIGN = -4,       /* pointer or stride misaligned */
+  CARNATOR_E_WORKSPACE = -5,   /* workspace NULL or smaller than required */
+  CARNATOR_E_HIP = -6          /* a HIP launch or runtime call failed */
+} carnator_status;
+
+/* Problem shape.  seq_len is the number of valid tokens N. */
+typedef struct {
+  int32_t batch;
+  int32_t heads;
+  int32_t seq_len;
+  int32_t head_dim; /* 64 or 128 */
+  int32_t block;    /* 64 or 128 */
+} carnator_shape;
+
+/* A bf16 [B, H, N, d] tensor: element strides, d contiguous. */
+typedef struct {
+  const void *data;
+  int64_t stride_b;
+  int64_t stride_h;
+  int64_t stride_n;
+} carnator_view;
+
+/* ABI version of the loaded library (CARNATOR_ABI_VERSION). */
+int carnator_abi_version(void);
+
+/* Static text of a status code (host). */
+const char *carnator_status_str(int status);
+
+/* Detail of the last failure on the calling thread (host); "" if none. */
+const char *carnator_last_error(void);
+
+/*
+ * Historical block connectivity -- Appendix C.3 ("Reuse-Scope
+ * Implementation Details"): for each head and query block, keep the smallest
+ * set of key blocks covering a fixed fraction of the attention mass.
+ *
+ * The mass of key block j for query block i is the softmax over j of the
+ * pooled logit s_ij = sigma * <mean_i(Q_hist), mean_j(K_hist)>, means over
+ * the valid tokens of each block, sigma = scale, or 1/sqrt(head_dim) when
+ * scale <= 0.  Key blocks are taken in descending s (lower j first on
+ * equality) until the cumulative mass reaches mass_threshold; k is that
+ * count.  Blocks whose score lies within 1e-6 of the k-th score are tied and
+ * the lower block indices among them fill the remaining places.
+ * mass_threshold >= 1 keeps every block.  Pooling, scores, softmax and
+ * selection are computed in fp64.
+ *
+ *   q_hist, k_hist  bf16 views of the historical copy [B, H, N, d]
+ *   mask_out        uint8 [B, H, nB, nB], written with 0/1
+ *   workspace       device scratch of at least
+ *                   carnator_build_block_mask_workspace_size(shape) bytes,
+ *                   256-byte aligned
+ * Errors: E_NULL, E_SHAPE (any size < 1, mass_threshold <= 0 or NaN),
+ * E_UNSUPPORTED, E_ALIGN, E_WORKSPACE, E_HIP.
+ */
+size_t carnator_build_block_mask_workspace_size(const carnator_shape *shape);
+int carnator_build_block_mask(const carnator_view *q_hist, const carnator_view *k_hist,
+                              const carnator_shape *shape, float scale, double mass_threshold,
+                              uint8_t *mask_out, void *workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
+/*
+ * Target-specific widening -- Sec. 3.3 ("Joint Reuse in Intermediate
+ * Layers"): target-specific computation is preserved for the localized
+ * region, so its query blocks evaluate every key block.
+ *
+ *   mask         uint8 [B, H, nB, nB], updated in place:
+ *                M[b,h,i,j] = (M != 0) | row_flags[b,i] | col_flags[b,j]
+ *   target_rows  uint8 [B, nB]; nonzero widens query block i to a full row
+ *   dense_cols   uint8 [B, nB] or NULL; nonzero makes key block j a full
+ *                column (dense text tokens)
+ * The result is written as 0/1 bytes.  Errors: E_NULL, E_SHAPE, E_HIP.
+ */
+int carnator_merge_target_rows(uint8_t *mask, const carnator_shape *shape,
+                               const uint8_t *target_rows, const uint8_t *dense_cols,
+                               hipStream_t stream);
+
+/*
+ * Per-row lists of kept key blocks (the compacted list the sparse executor
+ * walks; rows are (b, h, i) in row-major order, R = B*H*nB).
+ *
+ *   mask      uint8 [B, H, nB, nB]
+ *   row_ptr   int32 [R + 1]; row r's list is col_idx[row_ptr[r] .. row_ptr[r+1])
+ *   col_idx   int32 [B*H*nB*nB] capacity; ascending key blocks per row
+ *   order     int32 [R]; rows by descending list length, lower row first on
+ *             equal length
+ *   workspace at least carnator_compact_block_mask_workspace_size(shape) bytes
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_WORKSPACE, E_HIP.
+ */
+size_t carnator_compact_block_mask_workspace_size(const carnator_shape *shape);
+int carnator_compact_block_mask(const uint8_t *mask, const carnator_shape *shape,
+                                int32_t *row_ptr, int32_t *col_idx, int32_t *order,
+                                void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Block-sparse attention -- Sec. 3.3 ("Historical Sparse-Connectivity
+ * Reuse") and Appendix C.3: the target's Q, K, V are recomputed and only the
+ * block pairs kept by the reused mask are evaluated.
+ *
+ * For a valid query token a in block i, with A(a) the keys t < N whose block
+ * is kept in row (b, h, i):
+ *   o_a = sum_{t in A(a)} softmax_t(sigma * q_a . k_t) v_t,
+ *   lse_a = log sum_{t in A(a)} exp(sigma * q_a . k_t),
+ * sigma = scale, or 1/sqrt(head_dim) when scale <= 0.  A row with no kept
+ * block gives o = 0 and lse = -inf.  bf16 matrix cores for Q.K^T and P.V,
+ * fp32 accumulation and online softmax; O is rounded to bf16.
+ *
+ *   q, k, v        bf16 views [B, H, N, d]
+ *   out            bf16 [B, H, N, d] at element strides out_stride_{b,h,n}
+ *                  (d contiguous); may not alias q, k or v
+ *   mask           uint8 [B, H, nB, nB]
+ *   lse            fp32 [B, H, N] contiguous, or NULL
+ *   workspace      at least carnator_block_sparse_attn_workspace_size(shape)
+ *                  bytes, 256-byte aligned (holds the compacted lists and a
+ *                  key-major copy of V)
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_WORKSPACE, E_HIP.
+ */
+size_t carnator_block_sparse_attn_workspace_size(const carnator_shape *shape);
+int carnator_block_sparse_attn(const carnator_view *q, const carnator_view *k,
+                               const carnator_view *v, void *out, int64_t out_stride_b,
+                               int64_t out_stride_h, int64_t out_stride_n,
+                               const carnator_shape *shape, const uint8_t *mask, float scale,
+                               float *lse, void *workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+
+/*
+ * Early-signature cosine scoring -- Sec. 3.1 (a target is compared against
+ * a bank built from completed requests) and Sec. 4.1 ("Candidate Recall":
+ * rank histories by similarity, keep the top K).
+ *
+ *   cos_m = <q, b_m> / (|q| |b_m|) accumulated in fp64; 0 when a norm is 0.
+ *   The top-k are taken in descending cosine (lower m first on equality);
+ *   among bank rows within 1e-6 of the k-th value the lower rows are kept.
+ *   idx_out lists the chosen rows in descending cosine, sim_out their values.
+ *
+ *   query        fp32 [nq, dim] contiguous
+ *   bank         fp32 [m, ld] row-major, ld >= dim
+ *   idx_out      int32 [nq, topk];  sim_out fp32 [nq, topk]
+ *   all_sim_out  fp32 [nq, m] or NULL (every cosine)
+ *   topk         1 .. min(m, 64)
+ *   workspace    at least carnator_signature_sim_workspace_size(nq, m, topk) bytes
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED (topk > 64), E_ALIGN, E_WORKSPACE, E_HIP.
+ */
+size_t carnator_signature_sim_workspace_size(int64_t nq, int64_t m, int32_t topk);
+int carnator_signature_sim(const float *query, int64_t nq, const float *bank, int64_t m,
+                           int64_t dim, int64_t ld, int32_t topk, int32_t *idx_out,
+                           float *sim_out, float *all_sim_out, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CARNATOR_H */

@@ -1,0 +1,253 @@
+"""Python binding of libcarnator (the C ABI in include/carnator.h).
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+libcarnator.so.  Tensors live on the GPU (PyTorch provides device memory and
+the current stream); outputs and workspaces are allocated with torch.empty.
+There is no CPU fallback: if the library is missing, importing the functions
+works but every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libcarnator.so")
+
+CARNATOR_OK = 0
+STATUS = {0: "OK", -1: "E_NULL", -2: "E_SHAPE", -3: "E_UNSUPPORTED", -4: "E_ALIGN",
+          -5: "E_WORKSPACE", -6: "E_HIP"}
+
+# Every entry point declared in include/carnator.h.
+EXPORTS = (
+    "carnator_abi_version", "carnator_status_str", "carnator_last_error",
+    "carnator_build_block_mask_workspace_size", "carnator_build_block_mask",
+    "carnator_merge_target_rows",
+    "carnator_compact_block_mask_workspace_size", "carnator_compact_block_mask",
+    "carnator_block_sparse_attn_workspace_size", "carnator_block_sparse_attn",
+    "carnator_signature_sim_workspace_size", "carnator_signature_sim",
+)
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("seq_len", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("block", ctypes.c_int32)]
+
+
+class View(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("stride_b", ctypes.c_int64), ("stride_h", ctypes.c_int64),
+                ("stride_n", ctypes.c_int64)]
+
+
+class CarnatorError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__("%s (%d): %s" % (STATUS.get(status, "?"), status, detail))
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libcarnator.so is not built (run python -m paper_2609_32420_amd.build)")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I32, I64, SZ, F32, F64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t,
+                                     ctypes.c_float, ctypes.c_double)
+        SP, VP = ctypes.POINTER(Shape), ctypes.POINTER(View)
+        sig = {
+            "carnator_abi_version": (ctypes.c_int, []),
+            "carnator_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+            "carnator_last_error": (ctypes.c_char_p, []),
+            "carnator_build_block_mask_workspace_size": (SZ, [SP]),
+            "carnator_build_block_mask": (ctypes.c_int, [VP, VP, SP, F32, F64, P, P, SZ, P]),
+            "carnator_merge_target_rows": (ctypes.c_int, [P, SP, P, P, P]),
+            "carnator_compact_block_mask_workspace_size": (SZ, [SP]),
+            "carnator_compact_block_mask": (ctypes.c_int, [P, SP, P, P, P, P, SZ, P]),
+            "carnator_block_sparse_attn_workspace_size": (SZ, [SP]),
+            "carnator_block_sparse_attn": (ctypes.c_int, [VP, VP, VP, P, I64, I64, I64, SP, P, F32, P, P,
+                                                          SZ, P]),
+            "carnator_signature_sim_workspace_size": (SZ, [I64, I64, I32]),
+            "carnator_signature_sim": (ctypes.c_int, [P, I64, P, I64, I64, I64, I32, P, P, P, P, SZ, P]),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != CARNATOR_OK:
+        raise CarnatorError(status, lib().carnator_last_error().decode())
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _shape(t: torch.Tensor, block: int) -> Shape:
+    B, H, N, d = t.shape
+    return Shape(B, H, N, d, block)
+
+
+def _view(t: torch.Tensor) -> View:
+    if t.dim() != 4 or t.dtype != torch.bfloat16 or not t.is_cuda or t.stride(3) != 1:
+        raise ValueError("expected a bf16 CUDA tensor [B, H, N, d] with d contiguous")
+    return View(t.data_ptr(), t.stride(0), t.stride(1), t.stride(2))
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator returns blocks aligned to at least 512 bytes
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def _dev_u8(x, device, shape) -> Optional[torch.Tensor]:
+    if x is None:
+        return None
+    x = torch.as_tensor(x, device=device)
+    if x.dtype != torch.uint8:
+        x = (x != 0).to(torch.uint8)
+    x = x.contiguous()
+    if tuple(x.shape) != tuple(shape):
+        raise ValueError("flags must have shape %s" % (tuple(shape),))
+    return x
+
+
+def abi_version() -> int:
+    return lib().carnator_abi_version()
+
+
+def build_block_mask_workspace(q_hist: torch.Tensor, block: int) -> torch.Tensor:
+    s = _shape(q_hist, block)
+    return _workspace(lib().carnator_build_block_mask_workspace_size(ctypes.byref(s)), q_hist.device)
+
+
+def build_block_mask(q_hist: torch.Tensor, k_hist: torch.Tensor, block: int, mass_threshold: float,
+                     scale: float = 0.0, out: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Historical block mask uint8 [B, H, nB, nB] (carnator_build_block_mask)."""
+    s = _shape(q_hist, block)
+    if tuple(k_hist.shape) != tuple(q_hist.shape):
+        raise ValueError("q_hist and k_hist shapes differ")
+    nb = -(-s.seq_len // block)
+    if out is None:
+        out = torch.empty(s.batch, s.heads, nb, nb, dtype=torch.uint8, device=q_hist.device)
+    L = lib()
+    ws = workspace if workspace is not None else build_block_mask_workspace(q_hist, block)
+    qv, kv = _view(q_hist), _view(k_hist)
+    _check(L.carnator_build_block_mask(ctypes.byref(qv), ctypes.byref(kv), ctypes.byref(s), float(scale),
+                                       float(mass_threshold), _ptr(out), _ptr(ws), ws.numel(),
+                                       _stream(q_hist)))
+    return out
+
+
+def merge_target_rows(mask: torch.Tensor, target_rows, dense_cols=None) -> torch.Tensor:
+    """Widens flagged query blocks to full rows (and flagged key blocks to full
+    columns) in place; returns ``mask``."""
+    B, H, nb, nb2 = mask.shape
+    if mask.dtype != torch.uint8 or not mask.is_contiguous() or nb != nb2:
+        raise ValueError("mask must be a contiguous uint8 [B, H, nB, nB] tensor")
+    rows = _dev_u8(target_rows, mask.device, (B, nb))
+    cols = _dev_u8(dense_cols, mask.device, (B, nb))
+    # any seq_len with this block count and a supported block size describes the mask
+    s = Shape(B, H, nb * 64, 64, 64)
+    _check(lib().carnator_merge_target_rows(_ptr(mask), ctypes.byref(s), _ptr(rows), _ptr(cols),
+                                            _stream(mask)))
+    return mask
+
+
+def compact_block_mask(mask: torch.Tensor):
+    """(row_ptr int32 [R+1], col_idx int32 [nnz], order int32 [R]).
+
+    Synchronises the stream once to size col_idx.
+    """
+    B, H, nb, _ = mask.shape
+    R = B * H * nb
+    s = Shape(B, H, nb * 64, 64, 64)
+    dev = mask.device
+    row_ptr = torch.empty(R + 1, dtype=torch.int32, device=dev)
+    col_idx = torch.empty(max(R * nb, 1), dtype=torch.int32, device=dev)
+    order = torch.empty(R, dtype=torch.int32, device=dev)
+    L = lib()
+    ws = _workspace(L.carnator_compact_block_mask_workspace_size(ctypes.byref(s)), dev)
+    _check(L.carnator_compact_block_mask(_ptr(mask.contiguous()), ctypes.byref(s), _ptr(row_ptr),
+                                         _ptr(col_idx), _ptr(order), _ptr(ws), ws.numel(), _stream(mask)))
+    nnz = int(row_ptr[-1].item())
+    return row_ptr, col_idx[:nnz], order
+
+
+def block_sparse_attn_workspace(q: torch.Tensor, block: int) -> torch.Tensor:
+    s = _shape(q, block)
+    return _workspace(lib().carnator_block_sparse_attn_workspace_size(ctypes.byref(s)), q.device)
+
+
+def block_sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, mask: torch.Tensor, block: int,
+                      scale: float = 0.0, return_lse: bool = False, out: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None):
+    """O = softmax(scale q k^T) v restricted to the kept block pairs
+    (carnator_block_sparse_attn).  Returns O (and the fp32 LSE)."""
+    s = _shape(q, block)
+    for t, n in ((k, "k"), (v, "v")):
+        if tuple(t.shape) != tuple(q.shape):
+            raise ValueError("%s shape differs from q" % n)
+    nb = -(-s.seq_len // block)
+    if tuple(mask.shape) != (s.batch, s.heads, nb, nb) or mask.dtype != torch.uint8 or not mask.is_contiguous():
+        raise ValueError("mask must be contiguous uint8 [B, H, nB, nB]")
+    if out is None:
+        out = torch.empty_like(q, memory_format=torch.contiguous_format)
+    lse = torch.empty(s.batch, s.heads, s.seq_len, dtype=torch.float32, device=q.device) if return_lse else None
+    L = lib()
+    if workspace is None:
+        workspace = block_sparse_attn_workspace(q, block)
+    qv, kv, vv = _view(q), _view(k), _view(v)
+    _check(L.carnator_block_sparse_attn(ctypes.byref(qv), ctypes.byref(kv), ctypes.byref(vv), _ptr(out),
+                                        out.stride(0), out.stride(1), out.stride(2), ctypes.byref(s),
+                                        _ptr(mask), float(scale), _ptr(lse), _ptr(workspace),
+                                        workspace.numel(), _stream(q)))
+    return (out, lse) if return_lse else out
+
+
+def signature_sim_workspace(nq: int, m: int, topk: int, device) -> torch.Tensor:
+    return _workspace(lib().carnator_signature_sim_workspace_size(nq, m, topk), device)
+
+
+def signature_sim(query: torch.Tensor, bank: torch.Tensor, topk: int, return_all: bool = False,
+                  workspace: Optional[torch.Tensor] = None, out=None):
+    """Top-k cosine of each query row against the bank (carnator_signature_sim).
+
+    Returns (idx int32 [nq, k], sim fp32 [nq, k]) and, with return_all, every
+    cosine fp32 [nq, M].  ``out`` may pass preallocated (idx, sim).
+    """
+    if query.dim() == 1:
+        query = query[None]
+    if query.dtype != torch.float32 or bank.dtype != torch.float32 or bank.dim() != 2:
+        raise ValueError("query [nq, D] and bank [M, ld] must be fp32")
+    if not query.is_contiguous() or bank.stride(1) != 1:
+        raise ValueError("query must be contiguous and bank rows contiguous")
+    nq, dim = query.shape
+    m = bank.shape[0]
+    dev = query.device
+    if out is not None:
+        idx, sim = out
+    else:
+        idx = torch.empty(nq, topk, dtype=torch.int32, device=dev)
+        sim = torch.empty(nq, topk, dtype=torch.float32, device=dev)
+    allsim = torch.empty(nq, m, dtype=torch.float32, device=dev) if return_all else None
+    L = lib()
+    if workspace is None:
+        workspace = signature_sim_workspace(nq, m, topk, dev)
+    _check(L.carnator_signature_sim(_ptr(query), nq, _ptr(bank), m, dim, bank.stride(0), int(topk), _ptr(idx),
+                                    _ptr(sim), _ptr(allsim), _ptr(workspace), workspace.numel(), _stream(query)))
+    return (idx, sim, allsim) if return_all else (idx, sim)

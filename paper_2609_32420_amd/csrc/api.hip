@@ -1,0 +1,280 @@
+// C ABI of the cache-hit block-sparse attention path (declared in
+// include/carnator.h): argument checks, workspace layout and launches.
+// Every check runs before the first HIP call, so a rejected call enqueues
+// nothing and writes nothing.
+#include "carnator.h"
+#include "internal.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+using namespace carnator;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return CARNATOR_OK;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+  return fail(CARNATOR_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int kMaxBlocks = 2048;  // nB limit of the selection kernel
+
+int check_shape(const carnator_shape *s) {
+  if (!s) return fail(CARNATOR_E_NULL, "shape is NULL");
+  if (s->batch < 1 || s->heads < 1 || s->seq_len < 1)
+    return fail(CARNATOR_E_SHAPE, "batch, heads and seq_len must be >= 1 (got %d, %d, %d)",
+                s->batch, s->heads, s->seq_len);
+  if (s->head_dim != 64 && s->head_dim != 128)
+    return fail(CARNATOR_E_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", s->head_dim);
+  if (s->block != 64 && s->block != 128)
+    return fail(CARNATOR_E_UNSUPPORTED, "block must be 64 or 128 (got %d)", s->block);
+  const int64_t nB = ((int64_t)s->seq_len + s->block - 1) / s->block;
+  if (nB > kMaxBlocks)
+    return fail(CARNATOR_E_UNSUPPORTED, "seq_len/block gives %lld blocks; at most %d supported",
+                (long long)nB, kMaxBlocks);
+  if ((int64_t)s->batch * s->heads * nB * nB > (int64_t)INT32_MAX)
+    return fail(CARNATOR_E_SHAPE, "batch*heads*nB*nB exceeds 2^31-1");
+  return CARNATOR_OK;
+}
+
+int n_blocks(const carnator_shape *s) { return (s->seq_len + s->block - 1) / s->block; }
+
+int check_view(const carnator_view *v, const carnator_shape *s, const char *name) {
+  if (!v || !v->data) return fail(CARNATOR_E_NULL, "%s is NULL", name);
+  if (reinterpret_cast<uintptr_t>(v->data) % 16 != 0)
+    return fail(CARNATOR_E_ALIGN, "%s data must be 16-byte aligned", name);
+  if (v->stride_b % 8 || v->stride_h % 8 || v->stride_n % 8)
+    return fail(CARNATOR_E_ALIGN, "%s strides must be multiples of 8 elements", name);
+  if (v->stride_n < s->head_dim || v->stride_b < 0 || v->stride_h < 0)
+    return fail(CARNATOR_E_SHAPE, "%s strides out of range (stride_n >= head_dim, others >= 0)", name);
+  return CARNATOR_OK;
+}
+
+View to_view(const carnator_view *v) {
+  return View{static_cast<const uint16_t *>(v->data), v->stride_b, v->stride_h, v->stride_n};
+}
+
+int check_ws(const void *ws, size_t have, size_t need) {
+  if (need > 0 && !ws) return fail(CARNATOR_E_WORKSPACE, "workspace is NULL (%zu bytes needed)", need);
+  if (have < need) return fail(CARNATOR_E_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+  if (need > 0 && reinterpret_cast<uintptr_t>(ws) % kAlign != 0)
+    return fail(CARNATOR_E_ALIGN, "workspace must be %zu-byte aligned", kAlign);
+  return CARNATOR_OK;
+}
+
+// Attention workspace: compacted lists, compaction scratch and V^T.
+struct AttnWs {
+  size_t row_ptr, col_idx, order, scratch, vt, total;
+};
+
+AttnWs attn_layout(const carnator_shape *s) {
+  const int64_t nB = n_blocks(s);
+  const int64_t R = (int64_t)s->batch * s->heads * nB;
+  AttnWs w;
+  size_t off = 0;
+  w.row_ptr = off;
+  off += align_up((size_t)(R + 1) * 4);
+  w.col_idx = off;
+  off += align_up((size_t)(R * nB) * 4);
+  w.order = off;
+  off += align_up((size_t)R * 4);
+  w.scratch = off;
+  off += compact_scratch_bytes(R);
+  w.vt = off;
+  off += align_up((size_t)s->batch * s->heads * s->head_dim * nB * s->block * 2);
+  w.total = off;
+  return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+int carnator_abi_version(void) { return CARNATOR_ABI_VERSION; }
+
+const char *carnator_status_str(int status) {
+  switch (status) {
+    case CARNATOR_OK: return "ok";
+    case CARNATOR_E_NULL: return "null pointer";
+    case CARNATOR_E_SHAPE: return "bad shape";
+    case CARNATOR_E_UNSUPPORTED: return "unsupported configuration";
+    case CARNATOR_E_ALIGN: return "misaligned pointer or stride";
+    case CARNATOR_E_WORKSPACE: return "workspace missing or too small";
+    case CARNATOR_E_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char *carnator_last_error(void) { return g_err; }
+
+// ---------------------------------------------------------------- mask builder
+
+size_t carnator_build_block_mask_workspace_size(const carnator_shape *s) {
+  if (check_shape(s) != CARNATOR_OK) return 0;
+  const size_t per = align_up((size_t)s->batch * s->heads * n_blocks(s) * s->head_dim * sizeof(double));
+  return 2 * per;
+}
+
+int carnator_build_block_mask(const carnator_view *q_hist, const carnator_view *k_hist,
+                              const carnator_shape *s, float scale, double mass_threshold,
+                              uint8_t *mask_out, void *workspace, size_t ws_bytes,
+                              hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if ((rc = check_view(q_hist, s, "q_hist"))) return rc;
+  if ((rc = check_view(k_hist, s, "k_hist"))) return rc;
+  if (!mask_out) return fail(CARNATOR_E_NULL, "mask_out is NULL");
+  if (!(mass_threshold > 0.0)) return fail(CARNATOR_E_SHAPE, "mass_threshold must be > 0");
+  if (!isfinite(scale)) return fail(CARNATOR_E_SHAPE, "scale must be finite");
+  const int nB = n_blocks(s);
+  const int BH = s->batch * s->heads;
+  const size_t mask_bytes = (size_t)BH * nB * nB;
+  if (mass_threshold >= 1.0) {
+    // every block pair is kept; no workspace is touched
+    hipError_t e = launch_fill_ones(mask_out, mask_bytes, stream);
+    if (e != hipSuccess) return hip_fail(e, "fill");
+    return ok();
+  }
+  const size_t need = carnator_build_block_mask_workspace_size(s);
+  if ((rc = check_ws(workspace, ws_bytes, need))) return rc;
+  const size_t per = need / 2;
+  double *qbar = static_cast<double *>(workspace);
+  double *kbarT = reinterpret_cast<double *>(static_cast<char *>(workspace) + per);
+  const double sigma = scale > 0.f ? (double)scale : 1.0 / sqrt((double)s->head_dim);
+  hipError_t e = launch_pool(to_view(q_hist), to_view(k_hist), s->batch, s->heads, s->seq_len,
+                             s->head_dim, s->block, qbar, kbarT, stream);
+  if (e != hipSuccess) return hip_fail(e, "pool");
+  e = launch_select(qbar, kbarT, BH, nB, s->head_dim, sigma, mass_threshold, mask_out, stream);
+  if (e != hipSuccess) return hip_fail(e, "select");
+  return ok();
+}
+
+// ---------------------------------------------------------------- merge
+
+int carnator_merge_target_rows(uint8_t *mask, const carnator_shape *s, const uint8_t *target_rows,
+                               const uint8_t *dense_cols, hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if (!mask) return fail(CARNATOR_E_NULL, "mask is NULL");
+  if (!target_rows) return fail(CARNATOR_E_NULL, "target_rows is NULL");
+  hipError_t e = launch_merge(mask, s->batch, s->heads, n_blocks(s), target_rows, dense_cols, stream);
+  if (e != hipSuccess) return hip_fail(e, "merge");
+  return ok();
+}
+
+// ---------------------------------------------------------------- compaction
+
+size_t carnator_compact_block_mask_workspace_size(const carnator_shape *s) {
+  if (check_shape(s) != CARNATOR_OK) return 0;
+  return compact_scratch_bytes((int64_t)s->batch * s->heads * n_blocks(s));
+}
+
+int carnator_compact_block_mask(const uint8_t *mask, const carnator_shape *s, int32_t *row_ptr,
+                                int32_t *col_idx, int32_t *order, void *workspace,
+                                size_t ws_bytes, hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if (!mask || !row_ptr || !col_idx || !order)
+    return fail(CARNATOR_E_NULL, "mask, row_ptr, col_idx and order must be non-NULL");
+  if ((rc = check_ws(workspace, ws_bytes, carnator_compact_block_mask_workspace_size(s)))) return rc;
+  const int nB = n_blocks(s);
+  hipError_t e = launch_compact(mask, (int64_t)s->batch * s->heads * nB, nB, row_ptr, col_idx,
+                                order, workspace, stream);
+  if (e != hipSuccess) return hip_fail(e, "compact");
+  return ok();
+}
+
+// ---------------------------------------------------------------- attention
+
+size_t carnator_block_sparse_attn_workspace_size(const carnator_shape *s) {
+  if (check_shape(s) != CARNATOR_OK) return 0;
+  return attn_layout(s).total;
+}
+
+int carnator_block_sparse_attn(const carnator_view *q, const carnator_view *k,
+                               const carnator_view *v, void *out, int64_t osb, int64_t osh,
+                               int64_t osn, const carnator_shape *s, const uint8_t *mask,
+                               float scale, float *lse, void *workspace, size_t ws_bytes,
+                               hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if ((rc = check_view(q, s, "q"))) return rc;
+  if ((rc = check_view(k, s, "k"))) return rc;
+  if ((rc = check_view(v, s, "v"))) return rc;
+  if (!out) return fail(CARNATOR_E_NULL, "out is NULL");
+  if (!mask) return fail(CARNATOR_E_NULL, "mask is NULL");
+  if (reinterpret_cast<uintptr_t>(out) % 16 != 0)
+    return fail(CARNATOR_E_ALIGN, "out must be 16-byte aligned");
+  if (osb % 8 || osh % 8 || osn % 8) return fail(CARNATOR_E_ALIGN, "out strides must be multiples of 8");
+  if (osn < s->head_dim || osb < 0 || osh < 0) return fail(CARNATOR_E_SHAPE, "out strides out of range");
+  if (!isfinite(scale)) return fail(CARNATOR_E_SHAPE, "scale must be finite");
+  const AttnWs L = attn_layout(s);
+  if ((rc = check_ws(workspace, ws_bytes, L.total))) return rc;
+  char *ws = static_cast<char *>(workspace);
+  int32_t *row_ptr = reinterpret_cast<int32_t *>(ws + L.row_ptr);
+  int32_t *col_idx = reinterpret_cast<int32_t *>(ws + L.col_idx);
+  int32_t *order = reinterpret_cast<int32_t *>(ws + L.order);
+  uint16_t *vt = reinterpret_cast<uint16_t *>(ws + L.vt);
+  const int nB = n_blocks(s);
+  const float sc = scale > 0.f ? scale : (float)(1.0 / sqrt((double)s->head_dim));
+  hipError_t e = launch_compact(mask, (int64_t)s->batch * s->heads * nB, nB, row_ptr, col_idx,
+                                order, ws + L.scratch, stream);
+  if (e != hipSuccess) return hip_fail(e, "compact");
+  e = launch_transpose_v(to_view(v), s->batch, s->heads, s->seq_len, s->head_dim, s->block, vt,
+                         stream);
+  if (e != hipSuccess) return hip_fail(e, "transpose_v");
+  e = launch_bsattn(to_view(q), to_view(k), vt, static_cast<uint16_t *>(out), osb, osh, osn,
+                    s->batch, s->heads, s->seq_len, s->head_dim, s->block, row_ptr, col_idx, order,
+                    sc, lse, stream);
+  if (e != hipSuccess) return hip_fail(e, "bsattn");
+  return ok();
+}
+
+// ---------------------------------------------------------------- signature scan
+
+size_t carnator_signature_sim_workspace_size(int64_t nq, int64_t m, int32_t topk) {
+  (void)topk;
+  if (nq < 1 || m < 1) return 0;
+  return align_up((size_t)nq * 8) + align_up((size_t)nq * m * 8);
+}
+
+int carnator_signature_sim(const float *query, int64_t nq, const float *bank, int64_t m,
+                           int64_t dim, int64_t ld, int32_t topk, int32_t *idx_out,
+                           float *sim_out, float *all_sim_out, void *workspace, size_t ws_bytes,
+                           hipStream_t stream) {
+  int rc;
+  if (!query || !bank || !idx_out || !sim_out)
+    return fail(CARNATOR_E_NULL, "query, bank, idx_out and sim_out must be non-NULL");
+  if (nq < 1 || m < 1 || dim < 1 || ld < dim)
+    return fail(CARNATOR_E_SHAPE, "need nq, m, dim >= 1 and ld >= dim");
+  if (m > INT32_MAX) return fail(CARNATOR_E_SHAPE, "m must fit in int32");
+  if (topk < 1 || topk > m) return fail(CARNATOR_E_SHAPE, "topk must be in [1, m]");
+  if (topk > 64) return fail(CARNATOR_E_UNSUPPORTED, "topk must be <= 64");
+  if (dim % 4 || ld % 4 || reinterpret_cast<uintptr_t>(query) % 16 || reinterpret_cast<uintptr_t>(bank) % 16)
+    return fail(CARNATOR_E_ALIGN, "dim and ld must be multiples of 4 and query/bank 16-byte aligned");
+  const size_t need = carnator_signature_sim_workspace_size(nq, m, topk);
+  if ((rc = check_ws(workspace, ws_bytes, need))) return rc;
+  double *qnorm = static_cast<double *>(workspace);
+  double *sims = reinterpret_cast<double *>(static_cast<char *>(workspace) + align_up((size_t)nq * 8));
+  hipError_t e = launch_sig(query, nq, bank, m, dim, ld, topk, idx_out, sim_out, all_sim_out, qnorm,
+                            sims, stream);
+  if (e != hipSuccess) return hip_fail(e, "signature_sim");
+  return ok();
+}
+
+}  // extern "C"

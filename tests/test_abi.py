@@ -1,0 +1,151 @@
+"""The C-ABI library: it loads, exports every symbol the header declares, and
+rejects bad arguments before any HIP call (so these run without a GPU)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2609_32420_amd as P
+from paper_2609_32420_amd import build as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "carnator.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(P.LIB_PATH):
+        B.build()
+    return P.lib()
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(carnator_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_python_export_list():
+    assert _declared() == sorted(P.EXPORTS)
+
+
+def test_every_declared_symbol_is_exported(L):
+    out = subprocess.run(["nm", "-D", "--defined-only", P.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (carnator_\w+)", out))
+    for name in _declared():
+        assert name in exported, name
+        assert getattr(L, name) is not None
+
+
+def test_abi_version_and_status_strings(L):
+    assert L.carnator_abi_version() == 1
+    assert L.carnator_status_str(0) == b"ok"
+    for code in (-1, -2, -3, -4, -5, -6):
+        assert L.carnator_status_str(code) not in (b"", b"unknown status")
+    assert L.carnator_status_str(12345) == b"unknown status"
+
+
+def _shape(B=1, H=2, N=192, d=64, bs=64):
+    return P.Shape(B, H, N, d, bs)
+
+
+def _view(ptr=0x10000, sb=0, sh=0, sn=64):
+    return P.View(ptr, sb, sh, sn)
+
+
+def test_workspace_sizes(L):
+    s = _shape(1, 12, 32760, 128, 128)
+    nb = 256
+    assert L.carnator_build_block_mask_workspace_size(ctypes.byref(s)) == 2 * 12 * nb * 128 * 8
+    ws = L.carnator_block_sparse_attn_workspace_size(ctypes.byref(s))
+    vt = 12 * 128 * nb * 128 * 2
+    assert ws >= vt + 12 * nb * nb * 4
+    assert L.carnator_signature_sim_workspace_size(1, 4096, 8) >= 4096 * 8
+    bad = _shape(d=96)
+    assert L.carnator_block_sparse_attn_workspace_size(ctypes.byref(bad)) == 0
+
+
+def _err(L):
+    return L.carnator_last_error().decode()
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("head_dim", 96, -3), ("block", 32, -3), ("batch", 0, -2), ("seq_len", 0, -2),
+    ("heads", -1, -2), ("seq_len", 2049 * 128, -3)])
+def test_build_mask_rejects_shapes(L, field, value, code):
+    s = _shape(bs=128, d=128)
+    setattr(s, field, value)
+    q = _view(sn=128)
+    r = L.carnator_build_block_mask(ctypes.byref(q), ctypes.byref(q), ctypes.byref(s), 0.0, 0.9,
+                                    ctypes.c_void_p(0x20000), ctypes.c_void_p(0x40000), 1 << 30, None)
+    assert r == code and _err(L)
+
+
+def test_build_mask_rejects_pointers_alignment_threshold_workspace(L):
+    s = _shape()
+    q = _view()
+    dst = ctypes.c_void_p(0x20000)
+    ws = ctypes.c_void_p(0x40000)
+    call = lambda qv, kv, tau, out, w, n: L.carnator_build_block_mask(
+        ctypes.byref(qv) if qv is not None else None, ctypes.byref(kv) if kv is not None else None,
+        ctypes.byref(s), 0.0, tau, out, w, n, None)
+    assert call(None, q, 0.9, dst, ws, 1 << 30) == -1
+    assert call(q, q, 0.9, None, ws, 1 << 30) == -1
+    assert call(_view(ptr=0x10008), q, 0.9, dst, ws, 1 << 30) == -4
+    assert call(_view(sn=60), q, 0.9, dst, ws, 1 << 30) == -4
+    assert call(_view(sn=56), q, 0.9, dst, ws, 1 << 30) == -2
+    assert call(q, q, 0.0, dst, ws, 1 << 30) == -2
+    assert call(q, q, float("nan"), dst, ws, 1 << 30) == -2
+    assert call(q, q, 0.9, dst, None, 1 << 30) == -5
+    assert call(q, q, 0.9, dst, ws, 16) == -5
+    assert call(q, q, 0.9, dst, ctypes.c_void_p(0x40010), 1 << 30) == -4
+    assert "workspace" in _err(L)
+
+
+def test_attention_rejects_bad_arguments(L):
+    s = _shape()
+    q = _view()
+    out = ctypes.c_void_p(0x20000)
+    mask = ctypes.c_void_p(0x30000)
+    ws = ctypes.c_void_p(0x40000)
+
+    def call(o=out, osn=64, m=mask, w=ws, n=1 << 30, qv=q, scale=0.0):
+        return L.carnator_block_sparse_attn(ctypes.byref(qv), ctypes.byref(q), ctypes.byref(q), o, 0, 0, osn,
+                                            ctypes.byref(s), m, scale, None, w, n, None)
+    assert call(o=None) == -1
+    assert call(m=None) == -1
+    assert call(o=ctypes.c_void_p(0x20002)) == -4
+    assert call(osn=12) == -4
+    assert call(osn=32) == -2
+    assert call(w=None) == -5
+    assert call(n=100) == -5
+    assert call(qv=_view(ptr=0)) == -1
+    assert call(scale=float("inf")) == -2
+
+
+def test_merge_compact_signature_reject(L):
+    s = _shape()
+    assert L.carnator_merge_target_rows(None, ctypes.byref(s), ctypes.c_void_p(0x100), None, None) == -1
+    assert L.carnator_merge_target_rows(ctypes.c_void_p(0x100), ctypes.byref(s), None, None, None) == -1
+    assert L.carnator_merge_target_rows(ctypes.c_void_p(0x100), None, ctypes.c_void_p(0x100), None, None) == -1
+    p = ctypes.c_void_p(0x1000)
+    assert L.carnator_compact_block_mask(p, ctypes.byref(s), p, None, p, p, 1 << 20, None) == -1
+    assert L.carnator_compact_block_mask(p, ctypes.byref(s), p, p, p, p, 4, None) == -5
+    q = ctypes.c_void_p(0x10000)
+    sig = L.carnator_signature_sim
+    assert sig(None, 1, q, 8, 16, 16, 2, q, q, None, q, 1 << 20, None) == -1
+    assert sig(q, 1, q, 8, 16, 16, 9, q, q, None, q, 1 << 20, None) == -2
+    assert sig(q, 1, q, 100, 16, 16, 65, q, q, None, q, 1 << 20, None) == -3
+    assert sig(q, 1, q, 8, 16, 8, 2, q, q, None, q, 1 << 20, None) == -2
+    assert sig(q, 1, q, 8, 18, 20, 2, q, q, None, q, 1 << 20, None) == -4
+    assert sig(q, 1, q, 8, 16, 16, 2, q, q, None, q, 8, None) == -5
+
+
+def test_python_binding_raises_without_gpu_tensors():
+    import torch
+    x = torch.zeros(1, 1, 64, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        P.block_sparse_attn(x, x, x, torch.ones(1, 1, 1, 1, dtype=torch.uint8), 64)

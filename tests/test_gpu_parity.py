@@ -1,0 +1,352 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Masks, merged masks and compacted lists must match bit for bit (rows the
+oracle reports as fragile -- a decision within 1e-9 of a threshold -- may take
+any admissible value).  Attention must match within max-abs 2e-2 and relative
+L2 5e-3 on the valid tokens compared; top-k indices exactly and cosines within
+1e-6.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_32420_amd as P
+import synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+ATOL = 2e-2
+REL_L2 = 5e-3
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _inputs(wid, seed=0, heads=None):
+    wl = synth.WORKLOADS[wid]
+    _say("inputs", wl.name, "seed", seed, "heads", heads)
+    return wl, synth.attention_inputs(wl, seed=seed, device=DEV, heads=heads)
+
+
+def _oracle_mask(x, wl):
+    """Oracle mask, built one head at a time to bound host memory."""
+    B, H = x["q_hist"].shape[:2]
+    nb = wl.n_blocks
+    m = np.zeros((B, H, nb, nb), dtype=np.uint8)
+    fragile = {}
+    for h in range(H):
+        mh, rep = oracle.build_block_mask(oracle.to_f64(x["q_hist"][:, h:h + 1]),
+                                          oracle.to_f64(x["k_hist"][:, h:h + 1]), wl.block, wl.tau)
+        m[:, h] = mh[:, 0]
+        for (b, _, i) in rep["fragile"]:
+            fragile[(b, h, i)] = rep["scores"][(b, 0, i)]
+    return m, fragile
+
+
+def _assert_masks_equal(got, want, fragile, tau):
+    got = got.cpu().numpy()
+    bad = np.argwhere((got != want).any(axis=-1))
+    for (b, h, i) in bad:
+        key = (int(b), int(h), int(i))
+        assert key in fragile, "mask row %s differs (k gpu %d, oracle %d)" % (
+            key, got[b, h, i].sum(), want[b, h, i].sum())
+        alts = oracle.row_admissible_masks(fragile[key], tau)
+        assert any(np.array_equal(got[b, h, i] != 0, a) for a in alts), key
+    _say("mask rows compared:", got.shape[0] * got.shape[1] * got.shape[2], "fragile:", len(fragile),
+         "density: %.4f" % got.mean())
+
+
+def _compare_rows(o_gpu, o_ref, lse_gpu, lse_ref, rows, N, bs):
+    og = o_gpu.float().cpu().numpy()
+    diffs, refs = [], []
+    for (b, h, i) in rows:
+        a0, a1 = i * bs, min((i + 1) * bs, N)
+        diffs.append((og[b, h, a0:a1] - o_ref[b, h, a0:a1]).ravel())
+        refs.append(o_ref[b, h, a0:a1].ravel())
+        if lse_gpu is not None:
+            lg = lse_gpu[b, h, a0:a1].cpu().numpy().astype(np.float64)
+            lr = lse_ref[b, h, a0:a1]
+            fin = np.isfinite(lr)
+            assert (np.isneginf(lg) == np.isneginf(lr)).all()
+            if fin.any():
+                assert np.abs(lg[fin] - lr[fin]).max() <= 1e-3
+    d = np.concatenate(diffs)
+    r = np.concatenate(refs)
+    mx = float(np.abs(d).max()) if d.size else 0.0
+    rel = float(np.linalg.norm(d) / max(np.linalg.norm(r), 1e-30))
+    _say("attention rows %d  max|d| %.3e  relL2 %.3e" % (len(rows), mx, rel))
+    assert mx <= ATOL
+    assert rel <= REL_L2
+
+
+def _sample_rows(wl, merged, rows_flags, heads, n_random=32, seed=0):
+    """Every target row of head 0, seeded random rows, and the last block of
+    every head."""
+    nb = wl.n_blocks
+    rows = set()
+    for i in np.nonzero(rows_flags[0])[0]:
+        rows.add((0, 0, int(i)))
+    rng = np.random.default_rng(seed)
+    for _ in range(n_random):
+        rows.add((0, int(rng.integers(0, heads)), int(rng.integers(0, nb))))
+    for h in range(heads):
+        rows.add((0, h, nb - 1))
+    return sorted(rows)
+
+
+# ---------------------------------------------------------------- mask builder
+
+@pytest.mark.parametrize("wid", [0, 1, 2, 3, 4])
+def test_mask_builder_bit_exact(wid):
+    wl, x = _inputs(wid)
+    got = P.build_block_mask(x["q_hist"], x["k_hist"], wl.block, wl.tau)
+    torch.cuda.synchronize()
+    want, fragile = _oracle_mask(x, wl)
+    _assert_masks_equal(got, want, fragile, wl.tau)
+
+
+@pytest.mark.parametrize("tau", [0.3, 0.97, 1.0])
+def test_mask_builder_thresholds_and_explicit_scale(tau):
+    wl, x = _inputs(0, seed=3)
+    got = P.build_block_mask(x["q_hist"], x["k_hist"], wl.block, tau, scale=0.05)
+    torch.cuda.synchronize()
+    want, rep = oracle.build_block_mask(oracle.to_f64(x["q_hist"]), oracle.to_f64(x["k_hist"]), wl.block, tau,
+                                        scale=0.05)
+    fragile = {k: rep["scores"][k] for k in rep["fragile"]}
+    _assert_masks_equal(got, want, fragile, tau)
+
+
+@pytest.mark.parametrize("N,bs,d", [(50, 64, 64), (1000, 64, 128), (4100, 128, 64), (9000, 64, 64)])
+def test_mask_builder_ragged_random(N, bs, d):
+    g = torch.Generator(device=DEV).manual_seed(N)
+    qh = torch.randn(2, 3, N, d, generator=g, device=DEV).to(torch.bfloat16)
+    kh = (qh.float() + 0.3 * torch.randn(2, 3, N, d, generator=g, device=DEV)).to(torch.bfloat16)
+    got = P.build_block_mask(qh, kh, bs, 0.8)
+    torch.cuda.synchronize()
+    want, rep = oracle.build_block_mask(oracle.to_f64(qh), oracle.to_f64(kh), bs, 0.8)
+    fragile = {k: rep["scores"][k] for k in rep["fragile"]}
+    _assert_masks_equal(got, want, fragile, 0.8)
+
+
+def test_mask_builder_constant_input_ties():
+    # All pooled logits equal: k = ceil(tau * nB), the lowest blocks.
+    x = torch.ones(1, 1, 640, 64, dtype=torch.bfloat16, device=DEV)
+    got = P.build_block_mask(x, x, 64, 0.45).cpu().numpy()
+    assert (got[0, 0] == np.array([1] * 5 + [0] * 5, dtype=np.uint8)[None, :]).all()
+
+
+# ---------------------------------------------------------------- merge, compaction
+
+@pytest.mark.parametrize("wid", [1, 2, 4])
+def test_merge_bit_exact(wid):
+    wl = synth.WORKLOADS[wid]
+    rows, cols, _ = synth.region_flags(wl, 0)
+    m = synth.random_mask(1, 3, wl.n_blocks, 0.2, wid) * np.uint8(5)  # nonzero bytes other than 1
+    got = P.merge_target_rows(torch.as_tensor(m, device=DEV), rows, cols).cpu().numpy()
+    np.testing.assert_array_equal(got, oracle.merge_target_rows(m, rows, cols))
+
+
+@pytest.mark.parametrize("nb,density", [(3, 0.5), (139, 0.3), (256, 0.2), (931, 0.1)])
+def test_compaction_bit_exact(nb, density):
+    m = synth.random_mask(1, 5, nb, density, nb)
+    m[0, 1, 0] = 0
+    m[0, 2, 1] = 1
+    dm = torch.as_tensor(m, device=DEV)
+    rp, ci, order = P.compact_block_mask(dm)
+    wrp, wci, word = oracle.compact_mask(m)
+    np.testing.assert_array_equal(rp.cpu().numpy(), wrp)
+    np.testing.assert_array_equal(ci.cpu().numpy(), wci)
+    np.testing.assert_array_equal(order.cpu().numpy(), word)
+
+
+# ---------------------------------------------------------------- attention
+
+def test_attention_tiny_workload_full():
+    wl, x = _inputs(0)
+    want_mask, _ = _oracle_mask(x, wl)
+    merged = oracle.merge_target_rows(want_mask, x["row_flags"].cpu().numpy())
+    o, lse = P.block_sparse_attn(x["q"], x["k"], x["v"], torch.as_tensor(merged, device=DEV), wl.block,
+                                 return_lse=True)
+    torch.cuda.synchronize()
+    ro, rl = oracle.block_sparse_attention(oracle.to_f64(x["q"]), oracle.to_f64(x["k"]), oracle.to_f64(x["v"]),
+                                           merged, wl.block)
+    rows = [(0, h, i) for h in range(wl.heads) for i in range(wl.n_blocks)]
+    _compare_rows(o, ro, lse, rl, rows, wl.seq_len, wl.block)
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 4])
+def test_attention_sampled_rows(wid):
+    wl, x = _inputs(wid)
+    H = wl.heads
+    # the oracle mask of the historical copy, widened on the host
+    want_mask, _ = _oracle_mask(x, wl)
+    rows_flags = x["row_flags"].cpu().numpy()
+    cols = None if x["col_flags"] is None else x["col_flags"].cpu().numpy()
+    merged = oracle.merge_target_rows(want_mask, rows_flags, cols)
+    _say("merged density %.4f" % merged.mean())
+    o, lse = P.block_sparse_attn(x["q"], x["k"], x["v"], torch.as_tensor(merged, device=DEV), wl.block,
+                                 return_lse=True)
+    torch.cuda.synchronize()
+    rows = _sample_rows(wl, merged, rows_flags, H)
+    heads = sorted({h for (_, h, _) in rows})
+    o_ref = np.full(o.shape, np.nan)
+    l_ref = np.full(lse.shape, np.nan)
+    for h in heads:
+        hr = [(b, 0, i) for (b, hh, i) in rows if hh == h]
+        ro, rl = oracle.block_sparse_attention(oracle.to_f64(x["q"][:, h:h + 1]), oracle.to_f64(x["k"][:, h:h + 1]),
+                                               oracle.to_f64(x["v"][:, h:h + 1]), merged[:, h:h + 1], wl.block,
+                                               rows=hr)
+        o_ref[:, h] = ro[:, 0]
+        l_ref[:, h] = rl[:, 0]
+    _compare_rows(o, o_ref, lse, l_ref, rows, wl.seq_len, wl.block)
+
+
+@pytest.mark.parametrize("wid", [0, 1])
+def test_end_to_end_path(wid):
+    """GPU builder -> GPU merge -> GPU attention against the oracle chain."""
+    wl, x = _inputs(wid)
+    mask = P.build_block_mask(x["q_hist"], x["k_hist"], wl.block, wl.tau)
+    P.merge_target_rows(mask, x["row_flags"], x["col_flags"])
+    o = P.block_sparse_attn(x["q"], x["k"], x["v"], mask, wl.block)
+    torch.cuda.synchronize()
+    want_mask, fragile = _oracle_mask(x, wl)
+    assert not fragile
+    merged = oracle.merge_target_rows(want_mask, x["row_flags"].cpu().numpy())
+    np.testing.assert_array_equal(mask.cpu().numpy(), merged)
+    rows = _sample_rows(wl, merged, x["row_flags"].cpu().numpy(), min(wl.heads, 2), n_random=8)
+    ro, rl = oracle.block_sparse_attention(oracle.to_f64(x["q"][:, :2]), oracle.to_f64(x["k"][:, :2]),
+                                           oracle.to_f64(x["v"][:, :2]), merged[:, :2], wl.block,
+                                           rows=[r for r in rows if r[1] < 2])
+    _compare_rows(o, ro, None, None, [r for r in rows if r[1] < 2], wl.seq_len, wl.block)
+
+
+@pytest.mark.parametrize("N,bs,d", [(50, 64, 64), (64, 64, 128), (200, 128, 64), (333, 64, 128),
+                                    (1000, 128, 128), (2048, 64, 64)])
+def test_attention_ragged_shapes_and_dims(N, bs, d):
+    g = torch.Generator(device=DEV).manual_seed(7 + N)
+    q, k, v = (torch.randn(2, 2, N, d, generator=g, device=DEV).to(torch.bfloat16) for _ in range(3))
+    nb = -(-N // bs)
+    m = synth.random_mask(2, 2, nb, 0.5, N)
+    m[..., -1] = 1  # the partial tail block is visited by every row
+    o, lse = P.block_sparse_attn(q, k, v, torch.as_tensor(m, device=DEV), bs, return_lse=True)
+    torch.cuda.synchronize()
+    ro, rl = oracle.block_sparse_attention(oracle.to_f64(q), oracle.to_f64(k), oracle.to_f64(v), m, bs)
+    rows = [(b, h, i) for b in range(2) for h in range(2) for i in range(nb)]
+    _compare_rows(o, ro, lse, rl, rows, N, bs)
+
+
+def test_attention_empty_rows_and_explicit_scale():
+    N, bs, d = 512, 128, 128
+    g = torch.Generator(device=DEV).manual_seed(11)
+    q, k, v = (torch.randn(1, 2, N, d, generator=g, device=DEV).to(torch.bfloat16) for _ in range(3))
+    m = synth.random_mask(1, 2, 4, 0.5, 11)
+    m[0, 0, 2] = 0  # no kept block: zeros and -inf
+    m[0, 1, 0] = 0
+    m[0, 1, 3, :] = 1
+    o, lse = P.block_sparse_attn(q, k, v, torch.as_tensor(m, device=DEV), bs, scale=0.2, return_lse=True)
+    torch.cuda.synchronize()
+    assert (o[0, 0, 256:384] == 0).all() and torch.isneginf(lse[0, 0, 256:384]).all()
+    ro, rl = oracle.block_sparse_attention(oracle.to_f64(q), oracle.to_f64(k), oracle.to_f64(v), m, bs, scale=0.2)
+    _compare_rows(o, ro, lse, rl, [(0, h, i) for h in range(2) for i in range(4)], N, bs)
+
+
+def test_attention_strided_views():
+    # Q, K, V as [B, N, H, d] storage viewed as [B, H, N, d]; O into a strided view.
+    N, bs, d, H = 300, 64, 64, 3
+    g = torch.Generator(device=DEV).manual_seed(5)
+    base = [torch.randn(1, N, H, d, generator=g, device=DEV).to(torch.bfloat16) for _ in range(3)]
+    q, k, v = (t.permute(0, 2, 1, 3) for t in base)
+    nb = -(-N // bs)
+    m = synth.random_mask(1, H, nb, 0.6, 5)
+    m[..., 0] = 1
+    out_store = torch.zeros(1, N, H, d, dtype=torch.bfloat16, device=DEV)
+    out = out_store.permute(0, 2, 1, 3)
+    P.block_sparse_attn(q, k, v, torch.as_tensor(m, device=DEV), bs, out=out)
+    torch.cuda.synchronize()
+    ro, _ = oracle.block_sparse_attention(oracle.to_f64(q), oracle.to_f64(k), oracle.to_f64(v), m, bs)
+    _compare_rows(out, ro, None, None, [(0, h, i) for h in range(H) for i in range(nb)], N, bs)
+
+
+def test_attention_full_mask_matches_dense_reference():
+    # All rows target-specific: the sparse path reduces to dense attention.
+    N, bs, d = 640, 128, 128
+    g = torch.Generator(device=DEV).manual_seed(3)
+    q, k, v = (torch.randn(1, 2, N, d, generator=g, device=DEV).to(torch.bfloat16) for _ in range(3))
+    m = np.zeros((1, 2, 5, 5), np.uint8)
+    merged = P.merge_target_rows(torch.as_tensor(m, device=DEV), np.ones((1, 5), np.uint8))
+    o = P.block_sparse_attn(q, k, v, merged, bs)
+    ref = torch.nn.functional.scaled_dot_product_attention(q.double().cpu(), k.double().cpu(), v.double().cpu())
+    d_ = (o.double().cpu() - ref)
+    assert d_.abs().max().item() <= ATOL
+    assert (d_.norm() / ref.norm()).item() <= REL_L2
+
+
+def test_deterministic_repeat():
+    wl, x = _inputs(1, heads=2)
+    m1 = P.build_block_mask(x["q_hist"], x["k_hist"], wl.block, wl.tau)
+    m2 = P.build_block_mask(x["q_hist"], x["k_hist"], wl.block, wl.tau)
+    assert torch.equal(m1, m2)
+    P.merge_target_rows(m1, x["row_flags"])
+    o1 = P.block_sparse_attn(x["q"], x["k"], x["v"], m1, wl.block)
+    o2 = P.block_sparse_attn(x["q"], x["k"], x["v"], m1, wl.block)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+
+
+# ---------------------------------------------------------------- signature scan
+
+def _check_topk(idx, sim, q, bank, k):
+    wi, wv, frag = oracle.topk_cosine(q, bank, k)
+    gi = idx.cpu().numpy()
+    gv = sim.cpu().numpy().astype(np.float64)
+    for r in range(q.shape[0]):
+        if frag[r]:
+            assert set(gi[r]) == set(wi[r])
+        else:
+            assert gi[r].tolist() == wi[r].tolist()
+        assert np.abs(gv[r] - wv[r]).max() <= 1e-6
+
+
+def test_signature_bank_workload():
+    sig = synth.signature_inputs(device=DEV)
+    q, b = sig["query"], sig["bank"]
+    idx, sim, allsim = P.signature_sim(q, b, synth.SIG_TOPK, return_all=True)
+    torch.cuda.synchronize()
+    qn, bn = q.cpu().numpy(), b.cpu().numpy()
+    _check_topk(idx, sim, qn, bn, synth.SIG_TOPK)
+    assert int(idx[1, 0]) == sig["planted"]
+    ref = oracle.cosine_similarity(qn, bn)
+    assert np.abs(allsim.cpu().numpy() - ref).max() <= 1e-6
+
+
+@pytest.mark.parametrize("m,dim,ld,nq,k", [(1, 4, 4, 1, 1), (100, 64, 72, 6, 64), (5000, 256, 256, 3, 17)])
+def test_signature_shapes(m, dim, ld, nq, k):
+    g = torch.Generator(device=DEV).manual_seed(m)
+    bank_store = torch.randn(m, ld, generator=g, device=DEV)
+    bank = bank_store[:, :dim]
+    q = torch.randn(nq, dim, generator=g, device=DEV)
+    if m > 1:
+        bank_store[min(3, m - 1)] = 0.0  # zero-norm row scores 0
+    idx, sim = P.signature_sim(q, bank, k)
+    torch.cuda.synchronize()
+    _check_topk(idx, sim, q.cpu().numpy(), bank.cpu().numpy(), k)
+
+
+def test_signature_ties_lower_row():
+    # Row 7 is parallel to the query (cosine 1); the others sit 5e-11 below.
+    # Within 1e-6 of the cut every row is tied, so the three lowest rows win.
+    bank = torch.zeros(10, 8, device=DEV)
+    bank[:, 0] = 1.0
+    bank[7, 1] = 1e-5
+    q = torch.zeros(1, 8, device=DEV)
+    q[0, 0] = 1.0
+    q[0, 1] = 1e-5
+    idx, sim = P.signature_sim(q, bank, 3)
+    assert idx[0].tolist() == [0, 1, 2]
+    wi, _, _ = oracle.topk_cosine(q.cpu().numpy(), bank.cpu().numpy(), 3)
+    assert wi[0].tolist() == [0, 1, 2]
