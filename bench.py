@@ -81,6 +81,9 @@ def main():
     ap.add_argument("--workload", type=int, default=1)
     ap.add_argument("--sets", type=int, default=3, help="input sets rotated across steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="before timing, copy a buffer of this size once (a reference kernel of known "
+                         "traffic for hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -139,6 +142,13 @@ def main():
             ev["attn"].append((e[2], e[3]))
             ev["sig"].append((e[3], e[4]))
 
+    if args.copy_calibration_mib > 0:
+        nbytes = args.copy_calibration_mib << 20
+        src = torch.ones(nbytes, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for i in range(args.warmup):
         step(i, False)
     torch.cuda.synchronize()
