@@ -250,7 +250,7 @@ int carnator_block_sparse_attn(const carnator_view *q, const carnator_view *k,
 size_t carnator_signature_sim_workspace_size(int64_t nq, int64_t m, int32_t topk) {
   (void)topk;
   if (nq < 1 || m < 1) return 0;
-  return align_up((size_t)nq * 8) + align_up((size_t)nq * m * 8);
+  return align_up((size_t)nq * m * 8);
 }
 
 int carnator_signature_sim(const float *query, int64_t nq, const float *bank, int64_t m,
@@ -269,10 +269,9 @@ int carnator_signature_sim(const float *query, int64_t nq, const float *bank, in
     return fail(CARNATOR_E_ALIGN, "dim and ld must be multiples of 4 and query/bank 16-byte aligned");
   const size_t need = carnator_signature_sim_workspace_size(nq, m, topk);
   if ((rc = check_ws(workspace, ws_bytes, need))) return rc;
-  double *qnorm = static_cast<double *>(workspace);
-  double *sims = reinterpret_cast<double *>(static_cast<char *>(workspace) + align_up((size_t)nq * 8));
-  hipError_t e = launch_sig(query, nq, bank, m, dim, ld, topk, idx_out, sim_out, all_sim_out, qnorm,
-                            sims, stream);
+  double *sims = static_cast<double *>(workspace);
+  hipError_t e = launch_sig(query, nq, bank, m, dim, ld, topk, idx_out, sim_out, all_sim_out, sims,
+                            stream);
   if (e != hipSuccess) return hip_fail(e, "signature_sim");
   return ok();
 }

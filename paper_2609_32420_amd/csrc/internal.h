@@ -51,6 +51,6 @@ hipError_t launch_bsattn(View q, View k, const uint16_t *vt, uint16_t *out, int6
 // ---- signature scan ----------------------------------------------------------
 hipError_t launch_sig(const float *query, int64_t nq, const float *bank, int64_t m, int64_t dim,
                       int64_t ld, int topk, int32_t *idx, float *sim, float *all_sim,
-                      double *qnorm, double *sims, hipStream_t s);
+                      double *sims, hipStream_t s);
 
 }  // namespace carnator

@@ -17,15 +17,17 @@ __device__ inline double bf16_to_f64(uint32_t bits16) {
 }
 
 // One workgroup per (tensor, bh, block).  Thread t owns 8 consecutive
-// channels (one 16-byte chunk) of every G-th token of the block; the G partial
-// sums are combined in a fixed order so the result does not depend on timing.
+// channels (one 16-byte chunk) of every G-th token of the block.  The G
+// partial sums are combined in a fixed order (first across the lanes of a
+// wave that share a chunk, then across waves), so the result does not depend
+// on timing.
 template <int D>
 __global__ void __launch_bounds__(256) pool_kernel(View q, View k, int H, int N, int bs, int nB,
                                                    double *__restrict__ qbar,
                                                    double *__restrict__ kbarT) {
   constexpr int CPR = D / 8;         // 16-byte chunks per token
   constexpr int G = 256 / CPR;       // token groups
-  __shared__ double part[G][D + 1];  // +1: keeps the column reads conflict-free
+  __shared__ double part[4][D];      // one partial per wave
   const int blk = blockIdx.x;
   const int bh = blockIdx.y;
   const int which = blockIdx.z;  // 0: Q_hist, 1: K_hist
@@ -48,12 +50,19 @@ __global__ void __launch_bounds__(256) pool_kernel(View q, View k, int H, int N,
       acc[2 * e + 1] += bf16_to_f64(ww[e] >> 16);
     }
   }
+  // lanes l, l + CPR, l + 2 CPR, ... of a wave hold the same channels
 #pragma unroll
-  for (int e = 0; e < 8; ++e) part[g][c * 8 + e] = acc[e];
+  for (int o = CPR; o < 64; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] += __shfl_xor(acc[e], o);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane < CPR) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[wave][c * 8 + e] = acc[e];
+  }
   __syncthreads();
   for (int ch = threadIdx.x; ch < D; ch += 256) {
-    double s = 0.0;
-    for (int gg = 0; gg < G; ++gg) s += part[gg][ch];
+    const double s = ((part[0][ch] + part[1][ch]) + part[2][ch]) + part[3][ch];
     const double mean = s / (double)n;
     if (which == 0)
       qbar[((int64_t)bh * nB + blk) * D + ch] = mean;
@@ -132,41 +141,59 @@ __device__ inline double wave_sum(double x) {
   return x;
 }
 
-// One workgroup (4 waves) per (bh, R consecutive query blocks).  Phase 1
-// computes the R x nB pooled logits into LDS; phase 2 lets each wave select
-// R/4 rows.
+// One workgroup of 8 waves per (bh, R = 8 consecutive query blocks).
+// Phase 1 computes the R x nB pooled logits into LDS; phase 2 gives each wave
+// one row to select.
+constexpr int kSelThreads = 512;
 template <int D, int E, int R>
-__global__ void __launch_bounds__(256) select_kernel(const double *__restrict__ qbar,
-                                                     const double *__restrict__ kbarT, int nB,
-                                                     double sigma, double tau,
-                                                     uint8_t *__restrict__ mask) {
-  extern __shared__ double sc[];  // [R][nB]
+__global__ void __launch_bounds__(kSelThreads) select_kernel(const double *__restrict__ qbar,
+                                                             const double *__restrict__ kbarT, int nB,
+                                                             double sigma, double tau,
+                                                             uint8_t *__restrict__ mask) {
+  static_assert(R == 8, "one row per wave");
+  extern __shared__ double sc[];  // [R][nB] logits, then [R][D] pooled queries
   const int bh = blockIdx.y;
   const int r0 = blockIdx.x * R;
   const int nr = min(R, nB - r0);
   const double *qb = qbar + ((int64_t)bh * nB + r0) * D;
   const double *kt = kbarT + (int64_t)bh * D * nB;
 
-  // ---- phase 1: s_ij = sigma * <qbar_i, kbar_j>
-  for (int jj = threadIdx.x; jj < nB; jj += 256) {
-    double acc[R];
+  // ---- phase 1: s_ij = sigma * <qbar_i, kbar_j>.  The R pooled query rows
+  // sit in LDS; thread t owns rows 4 (t / 256) .. +4 of key blocks
+  // t % 256 + 256 u, and streams kbar^T[c][j] (coalesced across lanes) 16
+  // channels at a time so the loads overlap.
+  double *qs = sc + R * nB;
+  for (int x = threadIdx.x; x < R * D; x += kSelThreads) {
+    const int r = x / D;
+    qs[x] = qb[min(r, nr - 1) * D + (x - r * D)];
+  }
+  __syncthreads();
+  const int rg = (threadIdx.x >> 8) * 4;
+  for (int jj = threadIdx.x & 255; jj < nB; jj += 256) {
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    for (int c0 = 0; c0 < D; c0 += 16) {
+      double kv[16];
 #pragma unroll
-    for (int r = 0; r < R; ++r) acc[r] = 0.0;
-    for (int c = 0; c < D; ++c) {
-      const double kv = kt[(int64_t)c * nB + jj];
+      for (int u = 0; u < 16; ++u) kv[u] = kt[(int64_t)(c0 + u) * nB + jj];
 #pragma unroll
-      for (int r = 0; r < R; ++r) acc[r] = fma(qb[min(r, nr - 1) * D + c], kv, acc[r]);
+      for (int u = 0; u < 16; u += 2)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const double2 qv = *reinterpret_cast<const double2 *>(qs + (rg + r) * D + c0 + u);
+          acc[r] = fma(qv.x, kv[u], acc[r]);
+          acc[r] = fma(qv.y, kv[u + 1], acc[r]);
+        }
     }
 #pragma unroll
-    for (int r = 0; r < R; ++r)
-      if (r < nr) sc[r * nB + jj] = sigma * acc[r];
+    for (int r = 0; r < 4; ++r)
+      if (rg + r < nr) sc[(rg + r) * nB + jj] = sigma * acc[r];
   }
   __syncthreads();
 
-  // ---- phase 2: selection, one row at a time per wave
+  // ---- phase 2: selection, one row per wave
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  for (int r = wave; r < nr; r += 4) {
+  for (int r = wave; r < nr; r += kSelThreads / 64) {
     const double *row = sc + r * nB;
     uint8_t *out = mask + ((int64_t)bh * nB + r0 + r) * nB;
     double s[E];
@@ -274,27 +301,42 @@ template <int D, int R>
 static hipError_t launch_select_dr(const double *qbar, const double *kbarT, int BH, int nB,
                                    double sigma, double tau, uint8_t *mask, hipStream_t s) {
   dim3 grid((nB + R - 1) / R, BH);
-  const size_t lds = (size_t)R * nB * sizeof(double);
+  const size_t lds = (size_t)R * (nB + D) * sizeof(double);
   const int P = nB <= 64 ? 64 : (1 << (32 - __builtin_clz((unsigned)(nB - 1))));
+#define CARNATOR_LDS_ATTR(EE)                                                                     \
+  do {                                                                                            \
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&select_kernel<D, EE, R>),  \
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);     \
+    if (e != hipSuccess) return e;                                                                \
+  } while (0)
   switch (P / 64) {
-    case 1: hipLaunchKernelGGL((select_kernel<D, 1, R>), grid, dim3(256), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    case 2: hipLaunchKernelGGL((select_kernel<D, 2, R>), grid, dim3(256), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    case 4: hipLaunchKernelGGL((select_kernel<D, 4, R>), grid, dim3(256), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    case 8: hipLaunchKernelGGL((select_kernel<D, 8, R>), grid, dim3(256), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    case 16: hipLaunchKernelGGL((select_kernel<D, 16, R>), grid, dim3(256), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    case 32: hipLaunchKernelGGL((select_kernel<D, 32, R>), grid, dim3(256), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
+    case 1: CARNATOR_LDS_ATTR(1); break;
+    case 2: CARNATOR_LDS_ATTR(2); break;
+    case 4: CARNATOR_LDS_ATTR(4); break;
+    case 8: CARNATOR_LDS_ATTR(8); break;
+    case 16: CARNATOR_LDS_ATTR(16); break;
+    case 32: CARNATOR_LDS_ATTR(32); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef CARNATOR_LDS_ATTR
+  switch (P / 64) {
+    case 1: hipLaunchKernelGGL((select_kernel<D, 1, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
+    case 2: hipLaunchKernelGGL((select_kernel<D, 2, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
+    case 4: hipLaunchKernelGGL((select_kernel<D, 4, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
+    case 8: hipLaunchKernelGGL((select_kernel<D, 8, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
+    case 16: hipLaunchKernelGGL((select_kernel<D, 16, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
+    case 32: hipLaunchKernelGGL((select_kernel<D, 32, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-// 8 rows per workgroup keep the logits of nB <= 1024 within 64 KiB of LDS;
-// longer rows (up to 2048 blocks) use 4.
+// 8 query blocks per workgroup: their logits and pooled rows take
+// 64 * (nB + d) bytes of LDS (at most 139 KiB for nB = 2048, d = 128).
 template <int D>
 static hipError_t launch_select_d(const double *qbar, const double *kbarT, int BH, int nB,
                                   double sigma, double tau, uint8_t *mask, hipStream_t s) {
-  if (nB <= 1024) return launch_select_dr<D, 8>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
-  return launch_select_dr<D, 4>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
+  return launch_select_dr<D, 8>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
 }
 
 hipError_t launch_select(const double *qbar, const double *kbarT, int BH, int nB, int d,

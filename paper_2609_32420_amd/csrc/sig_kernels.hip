@@ -22,27 +22,15 @@ __device__ inline double wave_sum(double x) {
   return x;
 }
 
-// |q| for each query (one workgroup per query, fixed-order reduction).
-__global__ void __launch_bounds__(256) qnorm_kernel(const float *__restrict__ query, int64_t dim,
-                                                    double *__restrict__ qnorm) {
-  __shared__ double part[4];
-  const float *qp = query + (int64_t)blockIdx.x * dim;
-  double acc = 0.0;
-  for (int64_t c = threadIdx.x; c < dim; c += 256) {
-    const double x = qp[c];
-    acc = fma(x, x, acc);
-  }
-  acc = wave_sum(acc);
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
-  __syncthreads();
-  if (threadIdx.x == 0) qnorm[blockIdx.x] = sqrt(((part[0] + part[1]) + part[2]) + part[3]);
-}
-
-// One wave per bank row (grid-stride).  Scores queries [q0, q0 + nqc).
+// One wave per bank row (grid-stride).  Scores queries [q0, q0 + nqc).  The
+// wave streams the bank row and the query rows U float4 at a time per lane,
+// so the loads of a row are in flight together.  |q|^2 is accumulated in the
+// same pass (every wave computes it in the same order, so every wave gets the
+// same value) and no separate norm pass is needed.
+constexpr int kU = 4;
 __global__ void __launch_bounds__(256) scan_kernel(const float *__restrict__ query, int64_t q0,
                                                    int nqc, const float *__restrict__ bank,
                                                    int64_t m, int64_t dim, int64_t ld,
-                                                   const double *__restrict__ qnorm,
                                                    double *__restrict__ sims,
                                                    float *__restrict__ all_sim) {
   const int lane = threadIdx.x & 63;
@@ -51,36 +39,56 @@ __global__ void __launch_bounds__(256) scan_kernel(const float *__restrict__ que
   for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < m; r += nwaves) {
     const float4 *bp = reinterpret_cast<const float4 *>(bank + r * ld);
     double bb = 0.0;
-    double dot[kQChunk];
+    double dot[kQChunk], qq2[kQChunk];
 #pragma unroll
-    for (int qq = 0; qq < kQChunk; ++qq) dot[qq] = 0.0;
-    for (int64_t c = lane; c < d4; c += 64) {
-      const float4 x = bp[c];
-      const double x0 = x.x, x1 = x.y, x2 = x.z, x3 = x.w;
-      bb = fma(x0, x0, bb);
-      bb = fma(x1, x1, bb);
-      bb = fma(x2, x2, bb);
-      bb = fma(x3, x3, bb);
+    for (int qq = 0; qq < kQChunk; ++qq) dot[qq] = qq2[qq] = 0.0;
+    for (int64_t c0 = lane; c0 < d4; c0 += 64 * kU) {
+      float4 x[kU];
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int64_t c = c0 + 64 * u;
+        x[u] = c < d4 ? bp[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
 #pragma unroll
       for (int qq = 0; qq < kQChunk; ++qq) {
         if (qq < nqc) {
-          const float4 y = reinterpret_cast<const float4 *>(query + (q0 + qq) * dim)[c];
-          double d = dot[qq];
-          d = fma(x0, (double)y.x, d);
-          d = fma(x1, (double)y.y, d);
-          d = fma(x2, (double)y.z, d);
-          d = fma(x3, (double)y.w, d);
+          const float4 *qp = reinterpret_cast<const float4 *>(query + (q0 + qq) * dim);
+          float4 y[kU];
+#pragma unroll
+          for (int u = 0; u < kU; ++u) {
+            const int64_t c = c0 + 64 * u;
+            y[u] = c < d4 ? qp[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+          }
+          double d = dot[qq], n2 = qq2[qq];
+#pragma unroll
+          for (int u = 0; u < kU; ++u) {
+            d = fma((double)x[u].x, (double)y[u].x, d);
+            d = fma((double)x[u].y, (double)y[u].y, d);
+            d = fma((double)x[u].z, (double)y[u].z, d);
+            d = fma((double)x[u].w, (double)y[u].w, d);
+            n2 = fma((double)y[u].x, (double)y[u].x, n2);
+            n2 = fma((double)y[u].y, (double)y[u].y, n2);
+            n2 = fma((double)y[u].z, (double)y[u].z, n2);
+            n2 = fma((double)y[u].w, (double)y[u].w, n2);
+          }
           dot[qq] = d;
+          qq2[qq] = n2;
         }
       }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        bb = fma((double)x[u].x, (double)x[u].x, bb);
+        bb = fma((double)x[u].y, (double)x[u].y, bb);
+        bb = fma((double)x[u].z, (double)x[u].z, bb);
+        bb = fma((double)x[u].w, (double)x[u].w, bb);
+      }
     }
-    bb = wave_sum(bb);
-    const double bn = sqrt(bb);
+    const double bn = sqrt(wave_sum(bb));
 #pragma unroll
     for (int qq = 0; qq < kQChunk; ++qq) {
       if (qq < nqc) {
         const double d = wave_sum(dot[qq]);
-        const double den = qnorm[q0 + qq] * bn;
+        const double den = sqrt(wave_sum(qq2[qq])) * bn;
         const double sv = den > 0.0 ? d / den : 0.0;
         if (lane == qq) {
           sims[(q0 + qq) * m + r] = sv;
@@ -98,22 +106,33 @@ __device__ inline bool better(double va, int ia, double vb, int ib) {
 
 // One workgroup per query: k rounds of block-wide argmax (each round takes
 // the best element after the previous pick in that order), then the tie rule.
-__global__ void __launch_bounds__(256) topk_kernel(const double *__restrict__ sims, int64_t m,
-                                                   int topk, int32_t *__restrict__ idx_out,
-                                                   float *__restrict__ sim_out) {
+// The query's similarities are first copied to LDS when they fit
+// (m <= kTopkLds), so the rounds read LDS instead of re-reading memory.
+constexpr int kTopkLds = 8192;
+__global__ void __launch_bounds__(1024) topk_kernel(const double *__restrict__ sims, int64_t m,
+                                                    int topk, int32_t *__restrict__ idx_out,
+                                                    float *__restrict__ sim_out) {
+  extern __shared__ double vals[];  // [min(m, kTopkLds)]
   __shared__ double topv[64];
   __shared__ int topi[64];
-  __shared__ double wv[4];
-  __shared__ int wi[4];
+  __shared__ double wv[16];
+  __shared__ int wi[16];
   __shared__ int tsel[64];
-  const double *sv = sims + (int64_t)blockIdx.x * m;
+  constexpr int NT = 1024;
+  const double *gsv = sims + (int64_t)blockIdx.x * m;
+  const bool in_lds = m <= kTopkLds;
+  if (in_lds) {
+    for (int64_t x = threadIdx.x; x < m; x += NT) vals[x] = gsv[x];
+    __syncthreads();
+  }
+  const double *sv = in_lds ? vals : gsv;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   double pv = INFINITY;
   int pi = -1;
   for (int r = 0; r < topk; ++r) {
     double bv = -INFINITY;
     int bi = 0x7fffffff;
-    for (int64_t x = threadIdx.x; x < m; x += 256) {
+    for (int64_t x = threadIdx.x; x < m; x += NT) {
       const double v = sv[x];
       const int i = (int)x;
       const bool after = v < pv || (v == pv && i > pi);
@@ -139,7 +158,7 @@ __global__ void __launch_bounds__(256) topk_kernel(const double *__restrict__ si
     if (threadIdx.x == 0) {
       double cv = wv[0];
       int ci = wi[0];
-      for (int q = 1; q < 4; ++q)
+      for (int q = 1; q < NT / 64; ++q)
         if (better(wv[q], wi[q], cv, ci)) {
           cv = wv[q];
           ci = wi[q];
@@ -197,16 +216,16 @@ __global__ void __launch_bounds__(256) topk_kernel(const double *__restrict__ si
 
 hipError_t launch_sig(const float *query, int64_t nq, const float *bank, int64_t m, int64_t dim,
                       int64_t ld, int topk, int32_t *idx, float *sim, float *all_sim,
-                      double *qnorm, double *sims, hipStream_t s) {
-  hipLaunchKernelGGL(qnorm_kernel, dim3((unsigned)nq), dim3(256), 0, s, query, dim, qnorm);
+                      double *sims, hipStream_t s) {
   const int64_t waves = (m + 3) / 4;
   const unsigned grid = (unsigned)(waves < 8192 ? waves : 8192);
   for (int64_t q0 = 0; q0 < nq; q0 += kQChunk) {
     const int nqc = (int)((nq - q0) < kQChunk ? (nq - q0) : kQChunk);
     hipLaunchKernelGGL(scan_kernel, dim3(grid), dim3(256), 0, s, query, q0, nqc, bank, m, dim, ld,
-                       qnorm, sims, all_sim);
+                       sims, all_sim);
   }
-  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)nq), dim3(256), 0, s, sims, m, topk, idx, sim);
+  const size_t lds = (size_t)(m <= kTopkLds ? m : 0) * sizeof(double);
+  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)nq), dim3(1024), lds, s, sims, m, topk, idx, sim);
   return hipGetLastError();
 }
 
