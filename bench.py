@@ -45,7 +45,7 @@ def dense_flops(B, H, N, d) -> float:
     return 4.0 * d * B * H * float(N) * float(N)
 
 
-def cpu_baseline(wl, heads: int = 2):
+def cpu_baseline(wl, heads: int = 8):
     """The oracle, as it stands, on a bounded sample: every step of the path
     for ``heads`` heads of the workload (mask, widening, attention of all
     query blocks of those heads) plus the full signature scan."""
