@@ -176,8 +176,7 @@ int carnator_compact_block_mask(const uint8_t *mask, const carnator_shape *shape
  *   mask           uint8 [B, H, nB, nB]
  *   lse            fp32 [B, H, N] contiguous, or NULL
  *   workspace      at least carnator_block_sparse_attn_workspace_size(shape)
- *                  bytes, 256-byte aligned (holds the compacted lists and a
- *                  key-major copy of V)
+ *                  bytes, 256-byte aligned (holds the compacted lists)
  * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_WORKSPACE, E_HIP.
  */
 size_t carnator_block_sparse_attn_workspace_size(const carnator_shape *shape);

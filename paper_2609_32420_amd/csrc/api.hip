@@ -77,9 +77,9 @@ int check_ws(const void *ws, size_t have, size_t need) {
   return CARNATOR_OK;
 }
 
-// Attention workspace: compacted lists, compaction scratch and V^T.
+// Attention workspace: compacted lists and compaction scratch.
 struct AttnWs {
-  size_t row_ptr, col_idx, order, scratch, vt, total;
+  size_t row_ptr, col_idx, order, scratch, total;
 };
 
 AttnWs attn_layout(const carnator_shape *s) {
@@ -95,8 +95,6 @@ AttnWs attn_layout(const carnator_shape *s) {
   off += align_up((size_t)R * 4);
   w.scratch = off;
   off += compact_scratch_bytes(R);
-  w.vt = off;
-  off += align_up((size_t)s->batch * s->heads * s->head_dim * nB * s->block * 2);
   w.total = off;
   return w;
 }
@@ -229,16 +227,12 @@ int carnator_block_sparse_attn(const carnator_view *q, const carnator_view *k,
   int32_t *row_ptr = reinterpret_cast<int32_t *>(ws + L.row_ptr);
   int32_t *col_idx = reinterpret_cast<int32_t *>(ws + L.col_idx);
   int32_t *order = reinterpret_cast<int32_t *>(ws + L.order);
-  uint16_t *vt = reinterpret_cast<uint16_t *>(ws + L.vt);
   const int nB = n_blocks(s);
   const float sc = scale > 0.f ? scale : (float)(1.0 / sqrt((double)s->head_dim));
   hipError_t e = launch_compact(mask, (int64_t)s->batch * s->heads * nB, nB, row_ptr, col_idx,
                                 order, ws + L.scratch, stream);
   if (e != hipSuccess) return hip_fail(e, "compact");
-  e = launch_transpose_v(to_view(v), s->batch, s->heads, s->seq_len, s->head_dim, s->block, vt,
-                         stream);
-  if (e != hipSuccess) return hip_fail(e, "transpose_v");
-  e = launch_bsattn(to_view(q), to_view(k), vt, static_cast<uint16_t *>(out), osb, osh, osn,
+  e = launch_bsattn(to_view(q), to_view(k), to_view(v), static_cast<uint16_t *>(out), osb, osh, osn,
                     s->batch, s->heads, s->seq_len, s->head_dim, s->block, row_ptr, col_idx, order,
                     sc, lse, stream);
   if (e != hipSuccess) return hip_fail(e, "bsattn");

@@ -40,13 +40,10 @@ hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_p
                           int32_t *col_idx, int32_t *order, void *scratch, hipStream_t s);
 
 // ---- attention -------------------------------------------------------------
-// V [B,H,N,d] -> Vt [BH][d][nB*bs] (keys contiguous, zero past N).
-hipError_t launch_transpose_v(View v, int B, int H, int N, int d, int bs, uint16_t *vt,
-                              hipStream_t s);
-hipError_t launch_bsattn(View q, View k, const uint16_t *vt, uint16_t *out, int64_t osb,
-                         int64_t osh, int64_t osn, int B, int H, int N, int d, int bs,
-                         const int32_t *row_ptr, const int32_t *col_idx, const int32_t *order,
-                         float scale, float *lse, hipStream_t s);
+hipError_t launch_bsattn(View q, View k, View v, uint16_t *out, int64_t osb, int64_t osh,
+                         int64_t osn, int B, int H, int N, int d, int bs, const int32_t *row_ptr,
+                         const int32_t *col_idx, const int32_t *order, float scale, float *lse,
+                         hipStream_t s);
 
 // ---- signature scan ----------------------------------------------------------
 hipError_t launch_sig(const float *query, int64_t nq, const float *bank, int64_t m, int64_t dim,
