@@ -41,9 +41,18 @@ __global__ void __launch_bounds__(256) pool_kernel(View q, View k, int H, int N,
   double acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-  for (int r = g; r < n; r += G) {
-    const uint4 w = *reinterpret_cast<const uint4 *>(base + (int64_t)r * v.sn);
-    const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+  // All of this thread's tokens (at most RPT) are loaded before any is added,
+  // so a wave keeps RPT 16-byte loads in flight instead of one.
+  constexpr int RPT = 128 / G;
+  uint4 w[RPT];
+#pragma unroll
+  for (int u = 0; u < RPT; ++u) {
+    const int r = g + u * G;
+    w[u] = r < n ? *reinterpret_cast<const uint4 *>(base + (int64_t)r * v.sn) : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int u = 0; u < RPT; ++u) {
+    const uint32_t ww[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       acc[2 * e] += bf16_to_f64(ww[e] & 0xffffu);

@@ -324,7 +324,14 @@ def test_signature_bank_workload():
     assert np.abs(allsim.cpu().numpy() - ref).max() <= 1e-6
 
 
-@pytest.mark.parametrize("m,dim,ld,nq,k", [(1, 4, 4, 1, 1), (100, 64, 72, 6, 64), (5000, 256, 256, 3, 17)])
+@pytest.mark.parametrize("m,dim,ld,nq,k", [
+    (1, 4, 4, 1, 1), (100, 64, 72, 6, 64), (5000, 256, 256, 3, 17),
+    # every row in registers, candidate filter with k = 16, queries in passes of 4 + 1
+    (8192, 64, 64, 5, 16),
+    # more rows than the top-k keeps in registers
+    (9000, 128, 132, 2, 8),
+    # query rows too long to stage in LDS
+    (300, 40000, 40000, 2, 5)])
 def test_signature_shapes(m, dim, ld, nq, k):
     g = torch.Generator(device=DEV).manual_seed(m)
     bank_store = torch.randn(m, ld, generator=g, device=DEV)
@@ -337,10 +344,11 @@ def test_signature_shapes(m, dim, ld, nq, k):
     _check_topk(idx, sim, q.cpu().numpy(), bank.cpu().numpy(), k)
 
 
-def test_signature_ties_lower_row():
+@pytest.mark.parametrize("m", [10, 3000, 9000])
+def test_signature_ties_lower_row(m):
     # Row 7 is parallel to the query (cosine 1); the others sit 5e-11 below.
     # Within 1e-6 of the cut every row is tied, so the three lowest rows win.
-    bank = torch.zeros(10, 8, device=DEV)
+    bank = torch.zeros(m, 8, device=DEV)
     bank[:, 0] = 1.0
     bank[7, 1] = 1e-5
     q = torch.zeros(1, 8, device=DEV)
