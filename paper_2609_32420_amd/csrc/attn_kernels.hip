@@ -23,6 +23,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 namespace carnator {
 namespace {
 
@@ -33,34 +35,32 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-// Keys per stage and ring depth (see Cfg).
-constexpr int kStageKeys = 64;
-constexpr int kRing = 2;
-
 // s_waitcnt immediate: vmcnt(0) with expcnt and lgkmcnt left at their maxima.
 constexpr int kWaitVm0 = 0x0F70;
 
-// The stage ring is driven by hand: the direct loads, the wait for the oldest
-// stage and the barrier are written as inline assembly.  Issued through the
-// compiler builtin, a direct load makes every later LDS read look like it may
-// alias the transfer, and the compiler then drains all outstanding stages
-// (vmcnt(0)) before each barrier and each operand read, which removes the
-// prefetch.  Nothing else in this kernel uses M0.
+// The tile loads are driven by hand: the direct loads, the wait and the
+// barrier are written as inline assembly.  Issued through the compiler
+// builtin, a direct load makes every later LDS read look like it may alias
+// the transfer, and the compiler then drains all outstanding loads
+// (vmcnt(0)) before each operand read, which removes the prefetch.  Nothing
+// else in this kernel uses M0.
 //
-// 16 bytes per lane from `g` to LDS offset lds_off + 16 * lane (lds_off is
-// the same in every lane).
-__device__ inline void dma16(const void *g, unsigned lds_off) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g),
+// 16 bytes per lane from base + voff to LDS offset lds_off + 16 * lane; base
+// and lds_off are the same in every lane.
+__device__ inline void dma16(const void *base, unsigned voff, unsigned lds_off) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base),
                "s"(__builtin_amdgcn_readfirstlane(lds_off))
                : "memory");
 }
-// Wait until at most N direct loads of this wave are in flight and every LDS
-// read of this wave has returned, then meet the other waves.
-template <int N>
-__device__ inline void wait_then_barrier() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+// Wait until every direct load and LDS read of this wave has completed, then
+// meet the other waves.
+__device__ inline void wait_all_then_barrier() {
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
+
+// An empty use of x at this point of the instruction stream: keeps the
+// compiler from sinking the computation of x into a later basic block.
+__device__ inline void anchor(float x) { asm volatile("" ::"v"(x)); }
 
 // MFMA row -> key inside a 32-key tile: swap bits 2 and 3.
 __device__ inline int perm32(int rr) { return (rr & ~12) | ((rr & 4) << 1) | ((rr & 8) >> 1); }
@@ -78,24 +78,6 @@ __device__ inline float2 halves(float x) {
 // rescale of the output accumulators.
 constexpr float kRescaleSlack = 8.f;
 
-template <int D, int BS, int KT_ = kStageKeys, int NST_ = kRing>
-struct Cfg {
-  static constexpr int KT = KT_;              // keys per stage
-  static constexpr int NST = NST_;            // stages in the LDS ring
-  static constexpr int MT = KT / 32;          // 32-key MFMA tiles per stage
-  static constexpr int WAVES = BS / 32;
-  static constexpr int NT = 64 * WAVES;       // == 2 * BS
-  static constexpr int RB = D * 2;            // bytes per K or V row
-  static constexpr int CPR = D / 8;           // 16-byte chunks per row
-  static constexpr int TB = KT * RB;          // bytes of one K (or V) stage
-  static constexpr int STAGE = 2 * TB;
-  static constexpr int LDS = NST * STAGE;
-  static constexpr int LI = TB / 1024 / WAVES;  // 1-KiB direct loads per wave for K (and for V)
-  static constexpr int LIW = 2 * LI;            // direct loads per wave per stage
-  static_assert(TB % (1024 * WAVES) == 0, "stage split");
-  static_assert(NST >= 2 && NST <= 4, "ring depth");
-};
-
 // Chunk swizzles (16-byte chunk c of row r sits in slot c ^ swz(r)).
 // K: the 16 lanes of a bank cycle read rows 0..15 (permuted) at one chunk.
 template <int CPR>
@@ -110,8 +92,46 @@ __device__ inline int swz_v(int r) {
   else return 4 * ((r >> 1) & 1);
 }
 
-// Two waves per SIMD (two workgroups per CU).  WITH_LSE adds the exact fp32
-// row sum the log-sum-exp output needs.
+// Longest key-block list a row can have (the number of key blocks is
+// limited to this by the entry points).
+constexpr int kMaxListBlocks = 2048;
+
+template <int D, int BS>
+struct Cfg {
+  static constexpr int KT = BS / 2;               // keys per stage (two stages per block)
+  static constexpr int MT = KT / 32;              // 32-key MFMA tiles per stage
+  static constexpr int WAVES = BS / 32;
+  static constexpr int NT = 64 * WAVES;
+  static constexpr int RB = D * 2;                // bytes per K or V row
+  static constexpr int CPR = D / 8;               // 16-byte chunks per row
+  static constexpr int RPL = 1024 / RB;           // rows per 1-KiB direct load
+  static constexpr int TB = KT * RB;              // one K or V tile
+  static constexpr int LIST = 4 * TB;             // the row's key-block list follows the tiles
+  static constexpr int LDS = LIST + 4 * (kMaxListBlocks + 2);  // K slots 0, 1; V slots 0, 1; list
+  static constexpr int LI = TB / 1024 / WAVES;    // direct loads per wave per tile
+  static_assert(TB % (1024 * WAVES) == 0, "tile split");
+};
+
+// One workgroup per query block, 32 queries per wave, two waves per SIMD.
+//
+// A wave issues vector instructions while its own MFMAs execute, but two
+// waves sharing a SIMD overlap their MFMA and vector work far less, so the
+// overlap is built into each wave's instruction stream.  Iteration j:
+//   part A: O += V(j-1)^T P(j-1)^T on the matrix cores, interleaved with the
+//           softmax of S(j) (row max, and P for the first 32 keys);
+//   part B: S(j+1) = K(j+1) Q^T, first for keys 0..31 of the stage while P
+//           for keys 32..63 of S(j) is formed, then for keys 32..63 once
+//           those scores have been consumed.
+// Only P is double-buffered in registers (the scores are reused in place).
+//
+// K and V have two LDS slots each.  Iteration j waits for V(j-1) and K(j+1),
+// meets the other waves (after which K(j) and V(j-2) are no longer read) and
+// issues V(j) and K(j+2) into those slots.
+//
+// A grown running max only records alpha: the output accumulators are
+// rescaled at the start of the next iteration, since the P.V in flight in
+// this one still belongs to the old max.  This keeps the softmax free of
+// branches, so it shares one scheduling region with the MFMAs.
 template <int D, int BS, bool WITH_LSE>
 __global__ void __launch_bounds__(2 * BS, 2)
 bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, int64_t osh,
@@ -119,7 +139,7 @@ bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, i
               const int32_t *__restrict__ col_idx, const int32_t *__restrict__ order, float c2,
               float *__restrict__ lse) {
   using C = Cfg<D, BS>;
-  constexpr int KT = C::KT, NST = C::NST, MT = C::MT;
+  constexpr int KT = C::KT, MT = C::MT;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
 
   const int row = order[blockIdx.x];
@@ -128,11 +148,9 @@ bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, i
   const int b = bh / H, h = bh - b * H;
   const int e0 = row_ptr[row], e1 = row_ptr[row + 1];
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
   const int qtok = qb * BS + wave * 32 + l32;
-  const int tail = N - (nB - 1) * BS;
-  const int tail_st = (tail + KT - 1) / KT;
 
   // ---- Q fragment (B operand of S^T = K Q^T): query l32, channels 16t+8hh..+8
   bf16x8 qreg[D / 16];
@@ -145,7 +163,7 @@ bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, i
       qreg[t] = __builtin_bit_cast(bf16x8, w);
     }
   }
-  // the Q fragment is in registers before any stage load is issued
+  // the Q fragment is in registers before any tile load is issued
   __builtin_amdgcn_s_waitcnt(kWaitVm0);
 
   f32x16 oacc[D / 32];
@@ -153,27 +171,30 @@ bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, i
   for (int mo = 0; mo < D / 32; ++mo)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[mo][r] = 0.f;
-  float mrun = -INFINITY, lrun = 0.f, lexact = 0.f;
+  float mrun = -INFINITY, lrun = 0.f, lexact = 0.f, alpha = 1.f;
 
   const uint16_t *kbase = k.data + (int64_t)b * k.sb + (int64_t)h * k.sh;
   const uint16_t *vbase = v.data + (int64_t)b * v.sb + (int64_t)h * v.sh;
 
-  // ---- direct-load descriptors: the i-th 1-KiB load of this wave fills
-  // bytes [1024 n, 1024 n + 1024) of the K (V) stage, n = wave * LI + i; lane
-  // l writes 16 bytes at 1024 n + 16 l, i.e. row r, slot s, which holds chunk
-  // s ^ swz(r) of that key row.
-  int ldrow[C::LI];
-  int64_t koff[C::LI], voff[C::LI];
+  // ---- direct loads: the i-th 1-KiB load of this wave fills rows
+  // RPL (wave LI + i) .. + RPL of a tile; lane l writes 16 bytes at 16 l,
+  // i.e. row +lrow, slot `slot`, which holds chunk slot ^ swz(row).
+  // A tile always covers KT rows inside the tensor: a stage reaching past N
+  // loads the KT rows ending at N instead (and masks the keys outside the
+  // stage), and when N < KT the rows past N re-read row N - 1.  So one set
+  // of lane offsets serves every tile.
+  const int lrow = lane / (C::RB / 16), slot = lane % (C::RB / 16);
+  unsigned koff[C::LI], voff[C::LI];  // lane offsets of a tile, bytes
 #pragma unroll
   for (int i = 0; i < C::LI; ++i) {
-    const int byte = (wave * C::LI + i) * 1024 + lane * 16;
-    const int r = byte / C::RB, s = (byte % C::RB) / 16;
-    ldrow[i] = r;
-    koff[i] = (int64_t)r * k.sn + (s ^ swz_k<C::CPR>(r)) * 8;
-    voff[i] = (int64_t)r * v.sn + (s ^ swz_v<C::CPR>(r)) * 8;
+    const int r = C::RPL * (wave * C::LI + i) + lrow;
+    const int rr = min(r, N - 1);
+    koff[i] = (unsigned)(((int64_t)rr * k.sn + (slot ^ swz_k<C::CPR>(r)) * 8) * 2);
+    voff[i] = (unsigned)(((int64_t)rr * v.sn + (slot ^ swz_v<C::CPR>(r)) * 8) * 2);
   }
+  const int kmax = max(N - KT, 0);  // first row of the last full tile
 
-  // ---- operand-read lane offsets inside a stage
+  // ---- operand-read lane offsets inside a tile
   // K (A of S^T): row perm32(l32), chunk 2t + hh
   int kread[D / 16];
   {
@@ -185,179 +206,272 @@ bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, i
   // supplies row 8 hh + 4 rd + (i >> 2) (+16 t'), 4 columns at
   // 32 mo + 16 (g & 1) + 4 (i & 3); it receives V[key0 + 0..3][dv0 + i].
   int vread[D / 32];
-  int vrow_base;
   {
     const int g = lane >> 4, i = lane & 15;
     const int qr = i >> 2, p = i & 3;
-    vrow_base = (8 * hh + qr) * C::RB + C::TB;
     const int sw = swz_v<C::CPR>(qr);  // rows differ from qr only above bit 1
 #pragma unroll
     for (int mo = 0; mo < D / 32; ++mo) {
       const int col = 32 * mo + 16 * (g & 1) + 4 * p;
-      vread[mo] = (((col >> 3) ^ sw) << 4) + ((col & 7) << 1);
+      vread[mo] = 2 * C::TB + (8 * hh + qr) * C::RB + (((col >> 3) ^ sw) << 4) + ((col & 7) << 1);
     }
   }
 
-  auto nst = [&](int j) { return j == nB - 1 ? tail_st : BS / KT; };
-
-  // issue the direct loads of stage (ee, ss) into ring buffer `buf`
   const unsigned lds_base = (unsigned)(size_t)(__attribute__((address_space(3))) unsigned char *)lds;
-  auto issue = [&](int ee, int ss, int buf) {
-    const int k0 = col_idx[ee] * BS + ss * KT;
-    const unsigned kdst = lds_base + buf * C::STAGE + wave * C::LI * 1024;
-    const unsigned vdst = kdst + C::TB;
-    if (k0 + KT <= N) {
-      const uint16_t *kt = kbase + (int64_t)k0 * k.sn;
-      const uint16_t *vt = vbase + (int64_t)k0 * v.sn;
+  const unsigned wdst = lds_base + wave * C::LI * 1024;
+  // the direct loads of one tile: first row k0t (<= N - KT), LDS offset dst
+  auto tile_base = [&](const uint16_t *base, int64_t sn, int k0t) __attribute__((always_inline)) { return base + (int64_t)k0t * sn; };
+  auto issue_tile = [&](const uint16_t *tp, const unsigned (&off)[C::LI], unsigned dst) __attribute__((always_inline)) {
 #pragma unroll
-      for (int i = 0; i < C::LI; ++i) {
-        dma16(kt + koff[i], kdst + i * 1024);
-        dma16(vt + voff[i], vdst + i * 1024);
-      }
-    } else {
-      // partial last block: rows past N re-read row N-1 (finite values whose
-      // scores are masked below)
-#pragma unroll
-      for (int i = 0; i < C::LI; ++i) {
-        const int r = min(k0 + ldrow[i], N - 1) - ldrow[i];
-        dma16(kbase + (int64_t)r * k.sn + koff[i], kdst + i * 1024);
-        dma16(vbase + (int64_t)r * v.sn + voff[i], vdst + i * 1024);
-      }
-    }
+    for (int i = 0; i < C::LI; ++i) dma16(tp, off[i], dst + i * 1024);
   };
 
-  // ---- prologue: the first NST-1 stages
-  int el = e0, sl = 0, pend = 0, lbuf = 0;
-  auto advance = [&](int &ee, int &ss) {
-    if (++ss >= nst(col_idx[ee])) {
-      ++ee;
-      ss = 0;
-    }
-  };
-#pragma unroll
-  for (int p = 0; p < NST - 1; ++p) {
-    if (el < e1) {
-      issue(el, sl, lbuf);
-      advance(el, sl);
-      ++pend;
-      lbuf = (lbuf + 1) % NST;
-    }
-  }
-
-  int ec = e0, sc = 0, cbuf = 0;
-  while (ec < e1) {
-    // stage (ec, sc) has landed when at most (pend - 1) newer stages are in
-    // flight; after the barrier every wave's part of it is in LDS and the
-    // buffer computed last (the oldest) is free for the next load
-    if constexpr (NST >= 4) {
-      if (pend >= 3) wait_then_barrier<2 * C::LIW>();
-      else if (pend == 2) wait_then_barrier<C::LIW>();
-      else wait_then_barrier<0>();
-    } else if constexpr (NST == 3) {
-      if (pend >= 2) wait_then_barrier<C::LIW>();
-      else wait_then_barrier<0>();
-    } else {
-      wait_then_barrier<0>();
-    }
-    --pend;
-    if (el < e1) {
-      issue(el, sl, lbuf);
-      advance(el, sl);
-      ++pend;
-      lbuf = (lbuf + 1) % NST;
-    }
-
-    const int k0 = col_idx[ec] * BS + sc * KT;
-    const unsigned char *stage = lds + cbuf * C::STAGE;
-
-    // ---- S^T = K Q^T for KT keys x 32 queries (MT 32-key MFMA tiles)
-    f32x16 sacc[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[mt][r] = 0.f;
-#pragma unroll
-      for (int t = 0; t < D / 16; ++t) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(stage + kread[t] + mt * 32 * C::RB);
-        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[t], sacc[mt], 0, 0, 0);
-      }
-    }
-    // keys past N (only in the partial last block)
-    if (k0 + KT > N) {
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int g = r >> 2, i = r & 3;
-          const int key = 32 * mt + 16 * (g >> 1) + 8 * hh + 4 * (g & 1) + i;
-          if (k0 + key >= N) sacc[mt][r] = -INFINITY;
-        }
-    }
-
-    // ---- online softmax (exp2 domain, c2 = scale * log2 e)
-    float mloc = sacc[0][0];
+  // Stage of keys [k0, k0 + KT) reaching past N: its tile starts at
+  // k0t = min(k0, N - KT); keys of the tile before k0 (they belong to the
+  // previous stage) or at N and beyond are masked.
+  auto mask_tail = [&](f32x16 (&sacc)[MT], int k0) __attribute__((always_inline)) {
+    const int k0t = min(k0, kmax);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, sacc[mt][r]);
-    {
-      const float2 hv = halves(mloc);
-      mloc = fmaxf(hv.x, hv.y);
-    }
-    const float mtile = mloc * c2;
-    if (__ballot(mtile > mrun + kRescaleSlack)) {
-      const float mnew = fmaxf(mrun, mtile);
-      const float alpha = (mnew == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f(mrun - mnew);
+      for (int r = 0; r < 16; ++r) {
+        const int g = r >> 2, i = r & 3;
+        const int key = k0t + 32 * mt + 16 * (g >> 1) + 8 * hh + 4 * (g & 1) + i;
+        if (key < k0 || key >= N) sacc[mt][r] = -INFINITY;
+      }
+  };
+  auto rescale_o = [&]() __attribute__((always_inline)) {
+    if (__ballot(alpha != 1.f)) {
 #pragma unroll
       for (int mo = 0; mo < D / 32; ++mo)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[mo][r] *= alpha;
-      lrun *= alpha;
-      if constexpr (WITH_LSE) lexact *= alpha;
-      mrun = mnew;
+      alpha = 1.f;
     }
-    const float msub = (mrun == -INFINITY) ? 0.f : mrun;
-    // P is rounded to bf16 for the P.V product, and the row sum adds up the
-    // same rounded values (two at a time with v_dot2 against (1, 1)), so each
-    // output is an exact convex combination of V rows up to fp32
-    // accumulation: the rounding of P does not bias it.
-    bf16x8 pb[KT / 16];
-    float psum[2] = {0.f, 0.f}, esum[4] = {0.f, 0.f, 0.f, 0.f};
-    const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
+  };
+
+  // ---- the softmax of one stage, in chunks that the iteration spreads over
+  // its MFMA slots (exp2 domain, c2 = scale * log2 e).  P is rounded to bf16
+  // for the P.V product, and the row sum adds up the same rounded values (two
+  // at a time with v_dot2 against (1, 1)), so each output is an exact convex
+  // combination of V rows up to fp32 accumulation.
+  constexpr int SC = MT * 16;               // scores per lane per stage
+  constexpr int XA = MT == 1 ? SC : SC / 2;  // scores turned into P in part A
+  const bf16x2 ones = {(__bf16)1.f, (__bf16)1.f};
+  struct Soft {
+    float m0, m1, msub, ps0, ps1, es0, es1;
+  };
+  // max over scores [x, x + 4)
+  auto sm_max = [&](Soft &st, const f32x16 (&sc)[MT], int x) __attribute__((always_inline)) {
+    st.m0 = __builtin_fmaxf(__builtin_fmaxf(st.m0, sc[x >> 4][x & 15]), sc[(x + 1) >> 4][(x + 1) & 15]);
+    st.m1 = __builtin_fmaxf(__builtin_fmaxf(st.m1, sc[(x + 2) >> 4][(x + 2) & 15]), sc[(x + 3) >> 4][(x + 3) & 15]);
+    anchor(st.m0);
+    anchor(st.m1);
+  };
+  auto sm_alpha = [&](Soft &st) __attribute__((always_inline)) {
+    const float2 hv = halves(__builtin_fmaxf(st.m0, st.m1));
+    const float mtile = __builtin_fmaxf(hv.x, hv.y) * c2;
+    const bool grow = mtile > mrun + kRescaleSlack;
+    const float mnew = grow ? mtile : mrun;
+    // exp2(mrun - mnew): 1 without growth, 0 from an empty start
+    const float a = __builtin_amdgcn_exp2f(mnew == -INFINITY ? 0.f : mrun - mnew);
+    alpha *= a;
+    mrun = mnew;
+    lrun *= a;
+    if constexpr (WITH_LSE) lexact *= a;
+    st.msub = (mnew == -INFINITY) ? 0.f : mnew;
+    anchor(st.msub);
+    anchor(a);
+  };
+  // P for scores x, x + 1
+  auto sm_exp = [&](Soft &st, const f32x16 (&sc)[MT], bf16x8 (&pc)[KT / 16], int x) __attribute__((always_inline)) {
+    const float v0 = __builtin_amdgcn_exp2f(fmaf(sc[x >> 4][x & 15], c2, -st.msub));
+    const float v1 = __builtin_amdgcn_exp2f(fmaf(sc[(x + 1) >> 4][(x + 1) & 15], c2, -st.msub));
+    const bf16x2 pp = {(__bf16)v0, (__bf16)v1};
+    anchor(__builtin_bit_cast(float, pp));
+    pc[x >> 3][x & 7] = pp[0];
+    pc[x >> 3][(x & 7) + 1] = pp[1];
+    if (((x >> 1) & 1) == 0) st.ps0 = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, st.ps0, false);
+    else st.ps1 = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, st.ps1, false);
+    if constexpr (WITH_LSE) {
+      if (((x >> 1) & 1) == 0) st.es0 += v0 + v1;
+      else st.es1 += v0 + v1;
+    }
+  };
+  auto sm_done = [&](Soft &st) __attribute__((always_inline)) {
+    lrun += st.ps0 + st.ps1;
+    if constexpr (WITH_LSE) lexact += st.es0 + st.es1;
+    anchor(lrun);
+  };
+
+  constexpr int PF = 4;  // operand reads run this many MFMA slots ahead
+  // plain S^T = K Q^T into sacc from K slot KS (prologue)
+  auto qk_plain = [&](f32x16 (&sacc)[MT]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int tp = 0; tp < KT / 16; ++tp) {
+    for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-      for (int jj = 0; jj < 8; jj += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[tp >> 1][8 * (tp & 1) + jj], c2, -msub));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[tp >> 1][8 * (tp & 1) + jj + 1], c2, -msub));
-        const bf16x2 pp = {(__bf16)p0, (__bf16)p1};
-        pb[tp][jj] = pp[0];
-        pb[tp][jj + 1] = pp[1];
-        psum[(jj >> 1) & 1] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, psum[(jj >> 1) & 1], false);
-        if constexpr (WITH_LSE) {
-          esum[jj >> 1] += p0;
-          esum[jj >> 1] += p1;
+      for (int t = 0; t < D / 16; ++t) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(lds + kread[t] + mt * 32 * C::RB);
+        if (t == 0) sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[t], f32x16{}, 0, 0, 0);
+        else sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[t], sacc[mt], 0, 0, 0);
+      }
+    }
+  };
+
+  // ---- one iteration (VS: V slot of stage j-1, KS: K slot of stage j+1;
+  // HAS_PV false for j = 0).  The direct loads of V(j) (tile vtp into LDS
+  // vdst) and of K(j+2) (ktp, kdst) go one per MFMA slot at the start of
+  // part A: issued in one burst they stall the wave behind the vector memory
+  // queue, and issued late they are not there at the next iteration.
+  auto iterate = [&](auto has_pv, auto vs_c, auto ks_c, f32x16 (&sc)[MT], const bf16x8 (&pprev)[KT / 16],
+                     bf16x8 (&pcur)[KT / 16], const uint16_t *vtp, unsigned vdst, const uint16_t *ktp,
+                     unsigned kdst) __attribute__((always_inline)) {
+    constexpr bool HP = decltype(has_pv)::value;
+    constexpr int VS = decltype(vs_c)::value, KS = decltype(ks_c)::value;
+    constexpr int NPV = (KT / 16) * (D / 32);  // PV MFMAs
+    constexpr int NQK = MT * (D / 16);         // QK MFMAs
+    static_assert(NPV >= 2 * C::LI, "load slots");
+    Soft st{-INFINITY, -INFINITY, 0.f, 0.f, 0.f, 0.f, 0.f};
+    // part A: PV(j-1) | max, alpha, P for the first half of the scores
+    {
+      bf16x8 vf[NPV];
+      auto vrd = [&](int i) __attribute__((always_inline)) {
+        const int tp = i / (D / 32), mo = i % (D / 32);
+        const int base = vread[mo] + VS * C::TB + 16 * tp * C::RB;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(lds + base));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(lds + base + 4 * C::RB));
+        vf[i] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      };
+      // chunk plan over NPV slots: SC/4 max chunks, the alpha chunk and the
+      // exp pairs of part A (all of them when a stage is one 32-key tile,
+      // whose scores part B overwrites at once; else the first half)
+      constexpr int NCA = SC / 4 + 1 + XA / 2 + (MT == 1 ? 1 : 0);
+      if constexpr (HP) {
+#pragma unroll
+        for (int i = 0; i < PF; ++i) vrd(i);
+      }
+#pragma unroll
+      for (int sl = 0; sl < NPV; ++sl) {
+        if constexpr (HP) {
+          if (sl + PF < NPV) vrd(sl + PF);
+          const int tp = sl / (D / 32), mo = sl % (D / 32);
+          oacc[mo] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[sl], pprev[tp], oacc[mo], 0, 0, 0);
         }
+        if (sl < C::LI) dma16(vtp, voff[sl], vdst + sl * 1024);
+        else if (sl < 2 * C::LI) dma16(ktp, koff[sl - C::LI], kdst + (sl - C::LI) * 1024);
+#pragma unroll
+        for (int c = 0; c < NCA; ++c) {
+          if (c * NPV / NCA != sl) continue;
+          if (c < SC / 4) sm_max(st, sc, 4 * c);
+          else if (c == SC / 4) sm_alpha(st);
+          else if (c < SC / 4 + 1 + XA / 2) sm_exp(st, sc, pcur, 2 * (c - SC / 4 - 1));
+          else sm_done(st);
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    lrun += psum[0] + psum[1];
-    if constexpr (WITH_LSE) lexact += (esum[0] + esum[1]) + (esum[2] + esum[3]);
+    // part B: S(j+1) | P for the second half
+    {
+      bf16x8 kf[NQK];
+      auto krd = [&](int i) __attribute__((always_inline)) {
+        const int mt = i / (D / 16), t = i % (D / 16);
+        kf[i] = *reinterpret_cast<const bf16x8 *>(lds + kread[t] + KS * C::TB + mt * 32 * C::RB);
+      };
+#pragma unroll
+      for (int i = 0; i < PF; ++i) krd(i);
+      // the second half of the scores is consumed during the first QK tile
+      constexpr int NCB = MT == 1 ? 0 : (SC - XA) / 2 + 1;
+#pragma unroll
+      for (int sl = 0; sl < NQK; ++sl) {
+        if (sl + PF < NQK) krd(sl + PF);
 
-    // ---- O^T += V^T P^T over KT/16 key steps of 16
+        const int mt = sl / (D / 16), t = sl % (D / 16);
+        if (t == 0) sc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[sl], qreg[t], f32x16{}, 0, 0, 0);
+        else sc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[sl], qreg[t], sc[mt], 0, 0, 0);
+        constexpr int SB = (MT == 1 ? NQK : NQK / MT);  // slots before the last tile
 #pragma unroll
-    for (int tp = 0; tp < KT / 16; ++tp) {
-      const unsigned char *vrow = stage + vrow_base + 16 * tp * C::RB;
-#pragma unroll
-      for (int mo = 0; mo < D / 32; ++mo) {
-        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(vrow + vread[mo]));
-        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(vrow + 4 * C::RB + vread[mo]));
-        const bf16x8 av = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        oacc[mo] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[tp], oacc[mo], 0, 0, 0);
+        for (int c = 0; c < NCB; ++c) {
+          if (c * SB / NCB != sl) continue;
+          if (c < (SC - XA) / 2) sm_exp(st, sc, pcur, XA + 2 * c);
+          else sm_done(st);
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
+  };
 
-    advance(ec, sc);
-    cbuf = (cbuf + 1) % NST;
+  if (e1 > e0) {
+    f32x16 sc[MT];
+    bf16x8 pa[KT / 16], pb[KT / 16];
+    using T = std::true_type;
+    using F = std::false_type;
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    const int L = e1 - e0;  // key blocks of the row; stages 2b and 2b+1 are block b
+    int *list = reinterpret_cast<int *>(lds + C::LIST);
+    // prologue: K(0), K(1) (both halves of block 0), the row's list into LDS;
+    // S(0)
+    int blk0 = col_idx[e0];
+    int blk1 = L > 1 ? col_idx[e0 + 1] : 0;
+    {
+      const int k0 = blk0 * BS;
+      issue_tile(tile_base(kbase, k.sn, min(k0, kmax)), koff, wdst);
+      issue_tile(tile_base(kbase, k.sn, min(k0 + KT, kmax)), koff, wdst + C::TB);
+    }
+    for (int i = threadIdx.x; i < L; i += C::NT) list[i] = col_idx[e0 + i];
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    qk_plain(sc);
+    if (blk0 * BS + KT > N) mask_tail(sc, blk0 * BS);
+
+    // Stages come in pairs (both halves of block b): iteration 2b loads V(2b)
+    // (first half of block b) and K(2b+2) (first half of block b+1),
+    // iteration 2b+1 the second halves.  blk0 / blk1 hold blocks b and b+1;
+    // block b+2 is read from the LDS list one pair ahead.
+    auto pair = [&](auto first, int b) __attribute__((always_inline)) {
+      const int nxt = list[min(b + 2, L - 1)];
+      const bool more = b + 1 < L;
+      // even stage j = 2b
+      wait_all_then_barrier();
+      if constexpr (!decltype(first)::value) rescale_o();
+      {
+        const int kv = blk0 * BS;
+        const int kk = more ? blk1 * BS : 0;
+        iterate(std::integral_constant<bool, !decltype(first)::value>{}, I1{}, I1{}, sc, pb, pa,
+                tile_base(vbase, v.sn, min(kv, kmax)), wdst + 2 * C::TB,
+                tile_base(kbase, k.sn, min(kk, kmax)), wdst);
+        if (blk0 * BS + 2 * KT > N) mask_tail(sc, blk0 * BS + KT);  // S(2b+1)
+      }
+      // odd stage j = 2b+1
+      wait_all_then_barrier();
+      rescale_o();
+      {
+        const int kv = blk0 * BS + KT;
+        const int kk = more ? blk1 * BS + KT : 0;
+        iterate(T{}, I0{}, I0{}, sc, pa, pb, tile_base(vbase, v.sn, min(kv, kmax)), wdst + 3 * C::TB,
+                tile_base(kbase, k.sn, min(kk, kmax)), wdst + C::TB);
+        if (more && blk1 * BS + KT > N) mask_tail(sc, blk1 * BS);  // S(2b+2)
+      }
+      blk0 = blk1;
+      blk1 = __builtin_amdgcn_readfirstlane(nxt);
+    };
+    pair(T{}, 0);
+    for (int b = 1; b < L; ++b) pair(F{}, b);
+    // P.V of the last stage (odd: V slot 1, P in pb)
+    wait_all_then_barrier();
+    rescale_o();
+    auto pv_last = [&](auto vs_c, const bf16x8 (&pl)[KT / 16]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int tp = 0; tp < KT / 16; ++tp)
+#pragma unroll
+        for (int mo = 0; mo < D / 32; ++mo) {
+          const int base = vread[mo] + decltype(vs_c)::value * C::TB + 16 * tp * C::RB;
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(lds + base));
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(lds + base + 4 * C::RB));
+          const bf16x8 av = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          oacc[mo] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pl[tp], oacc[mo], 0, 0, 0);
+        }
+    };
+    pv_last(I1{}, pb);
   }
 
   // ---- epilogue: normalise, store bf16 O (and the LSE)
