@@ -4,8 +4,10 @@ One step = the four rows of the path on one batch of synthetic input that is
 already resident in HBM:
   1. historical block mask from pooled Q_hist.K_hist (carnator_build_block_mask)
   2. target-row widening (carnator_merge_target_rows)
-  3. block-sparse attention of the target Q, K, V (carnator_block_sparse_attn,
-     which also compacts the mask)
+  3. block-sparse attention of the target Q, K, V: the mask compacted into
+     per-row block lists (carnator_compact_block_mask), then the attention
+     kernel from those lists (carnator_block_sparse_attn_lists; the same two
+     steps carnator_block_sparse_attn runs in one call)
   4. Early-Signature cosine top-k against the 4096 x 3072 bank
      (carnator_signature_sim)
 Three input sets are rotated so the 256 MB Infinity Cache does not serve
@@ -13,7 +15,12 @@ repeated reads of the HBM-bound steps.
 
 Prints one JSON line.  ``value`` is executed attention TFLOP per step divided
 by the step time (whole-job throughput); ``roofline`` describes the attention
-kernel against the bf16 MFMA peak.
+kernel (one launch, timed with events on its stream) against the bf16 MFMA
+peak.  ``roofline.traffic`` is the kernel's HBM traffic per launch from
+rocprofv3 FETCH_SIZE / WRITE_SIZE passes, scaled by the same counters on a
+copy of known size (paper_2609_32420_amd/measured_traffic.json); it is null
+when the kernel source no longer matches the one those counters were taken
+on.
 """
 import argparse
 import json
@@ -43,6 +50,25 @@ def executed_flops(mask: np.ndarray, N: int, bs: int, d: int) -> float:
 
 def dense_flops(B, H, N, d) -> float:
     return 4.0 * d * B * H * float(N) * float(N)
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "paper_2609_32420_amd", "measured_traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_32420_amd", "csrc", "attn_kernels.hip")
+
+
+def measured_traffic(d: int, bs: int):
+    """HBM bytes per launch of the attention kernel from the recorded
+    FETCH_SIZE / WRITE_SIZE passes, or None when there is no record for this
+    configuration or the kernel source changed since it was taken."""
+    import hashlib
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+        src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256") != src or rec.get("head_dim") != d or rec.get("block") != bs:
+        return None
+    return rec.get("bytes_per_launch")
 
 
 def cpu_baseline(wl, heads: int = 8):
@@ -109,7 +135,11 @@ def main():
     # persistent outputs and workspaces: nothing is allocated inside the timed region
     masks = [torch.empty(B, H, nb, nb, dtype=torch.uint8, device=dev) for _ in sets]
     outs = [torch.empty(B, H, N, d, dtype=torch.bfloat16, device=dev) for _ in sets]
-    ws_attn = P.block_sparse_attn_workspace(sets[0][0]["q"], bs)
+    ws_cmp = P.compact_block_mask_workspace(masks[0])
+    R = B * H * nb
+    lists = (torch.empty(R + 1, dtype=torch.int32, device=dev),
+             torch.empty(R * nb, dtype=torch.int32, device=dev),
+             torch.empty(R, dtype=torch.int32, device=dev))
     ws_mask = P.build_block_mask_workspace(sets[0][0]["q_hist"], bs)
     ws_sig = P.signature_sim_workspace(synth.SIG_NQ, synth.SIG_M, synth.SIG_TOPK, dev)
     sig_out = (torch.empty(synth.SIG_NQ, synth.SIG_TOPK, dtype=torch.int32, device=dev),
@@ -117,12 +147,12 @@ def main():
     flags = [(x["row_flags"].contiguous(), None if x["col_flags"] is None else x["col_flags"].contiguous())
              for x, _ in sets]
 
-    ev = {k: [] for k in ("build", "merge", "attn", "sig")}
+    ev = {k: [] for k in ("build", "merge", "compact", "attn", "sig")}
 
     def step(i, record):
         si = i % len(sets)
         x, sg = sets[si]
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(5)] if record else None
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(6)] if record else None
         if record:
             e[0].record(stream)
         P.build_block_mask(x["q_hist"], x["k_hist"], bs, wl.tau, out=masks[si], workspace=ws_mask)
@@ -131,16 +161,18 @@ def main():
         P.merge_target_rows(masks[si], flags[si][0], flags[si][1])
         if record:
             e[2].record(stream)
-        P.block_sparse_attn(x["q"], x["k"], x["v"], masks[si], bs, out=outs[si], workspace=ws_attn)
+        P.compact_block_mask(masks[si], trim=False, out=lists, workspace=ws_cmp)
         if record:
             e[3].record(stream)
-        P.signature_sim(sg["query"], sg["bank"], synth.SIG_TOPK, workspace=ws_sig, out=sig_out)
+        P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists, bs, out=outs[si])
         if record:
             e[4].record(stream)
-            ev["build"].append((e[0], e[1]))
-            ev["merge"].append((e[1], e[2]))
-            ev["attn"].append((e[2], e[3]))
-            ev["sig"].append((e[3], e[4]))
+        P.signature_sim(sg["query"], sg["bank"], synth.SIG_TOPK, workspace=ws_sig, out=sig_out)
+        if record:
+            e[5].record(stream)
+            for k_, (a_, b_) in zip(("build", "merge", "compact", "attn", "sig"),
+                                    ((0, 1), (1, 2), (2, 3), (3, 4), (4, 5))):
+                ev[k_].append((e[a_], e[b_]))
 
     if args.copy_calibration_mib > 0:
         nbytes = args.copy_calibration_mib << 20
@@ -200,11 +232,13 @@ def main():
         "builder_GBps": round(builder_bytes / (build_ms * 1e-3) / 1e9, 1),
         "builder_pct_hbm_peak": round(100.0 * builder_bytes / (build_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 2),
         "merge_ms_per_call": round(avg_ms("merge"), 4),
+        "compact_ms_per_call": round(avg_ms("compact"), 4),
         "sig_ms_per_call": round(sig_ms, 4),
         "sig_GBps": round(sig_bytes / (sig_ms * 1e-3) / 1e9, 1),
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                     "kernel": "block_sparse_attn call (compaction + V transpose + attention kernel)"},
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic(d, bs),
+                     "kernel": "bsattn_kernel<%d, %d> (one launch of carnator_block_sparse_attn_lists)" % (d, bs)},
     }
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)

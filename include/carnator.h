@@ -188,6 +188,29 @@ int carnator_block_sparse_attn(const carnator_view *q, const carnator_view *k,
                                hipStream_t stream);
 
 /*
+ * Block-sparse attention from compacted lists -- the same operation as
+ * carnator_block_sparse_attn with the kept key blocks given as the lists
+ * carnator_compact_block_mask writes for the mask (for callers that reuse one
+ * mask for several calls, or time the attention kernel on its own).  One
+ * kernel launch, no workspace.
+ *
+ *   q, k, v, out, out strides, shape, scale, lse: as carnator_block_sparse_attn
+ *   row_ptr  int32 [R + 1], col_idx int32 (row lists, ascending), order
+ *            int32 [R] (a permutation of the R = B*H*nB rows, longest list
+ *            first): exactly as written by carnator_compact_block_mask
+ * The kernel clamps rows, list bounds and block indices into range, so
+ * malformed lists give wrong output but no access outside q, k, v, out,
+ * lse and the lists' documented extents.
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_HIP.
+ */
+int carnator_block_sparse_attn_lists(const carnator_view *q, const carnator_view *k,
+                                     const carnator_view *v, void *out, int64_t out_stride_b,
+                                     int64_t out_stride_h, int64_t out_stride_n,
+                                     const carnator_shape *shape, const int32_t *row_ptr,
+                                     const int32_t *col_idx, const int32_t *order, float scale,
+                                     float *lse, hipStream_t stream);
+
+/*
  * Early-signature cosine scoring -- Sec. 3.1 (a target is compared against
  * a bank built from completed requests) and Sec. 4.1 ("Candidate Recall":
  * rank histories by similarity, keep the top K).

@@ -28,6 +28,7 @@ EXPORTS = (
     "carnator_merge_target_rows",
     "carnator_compact_block_mask_workspace_size", "carnator_compact_block_mask",
     "carnator_block_sparse_attn_workspace_size", "carnator_block_sparse_attn",
+    "carnator_block_sparse_attn_lists",
     "carnator_signature_sim_workspace_size", "carnator_signature_sim",
 )
 
@@ -73,6 +74,8 @@ def lib() -> ctypes.CDLL:
             "carnator_block_sparse_attn_workspace_size": (SZ, [SP]),
             "carnator_block_sparse_attn": (ctypes.c_int, [VP, VP, VP, P, I64, I64, I64, SP, P, F32, P, P,
                                                           SZ, P]),
+            "carnator_block_sparse_attn_lists": (ctypes.c_int, [VP, VP, VP, P, I64, I64, I64, SP, P, P, P, F32,
+                                                                P, P]),
             "carnator_signature_sim_workspace_size": (SZ, [I64, I64, I32]),
             "carnator_signature_sim": (ctypes.c_int, [P, I64, P, I64, I64, I64, I32, P, P, P, P, SZ, P]),
         }
@@ -168,24 +171,42 @@ def merge_target_rows(mask: torch.Tensor, target_rows, dense_cols=None) -> torch
     return mask
 
 
-def compact_block_mask(mask: torch.Tensor):
-    """(row_ptr int32 [R+1], col_idx int32 [nnz], order int32 [R]).
+def compact_block_mask_workspace(mask: torch.Tensor) -> torch.Tensor:
+    B, H, nb, _ = mask.shape
+    s = Shape(B, H, nb * 64, 64, 64)
+    return _workspace(lib().carnator_compact_block_mask_workspace_size(ctypes.byref(s)), mask.device)
 
-    Synchronises the stream once to size col_idx.
+
+def compact_block_mask(mask: torch.Tensor, trim: bool = True, out=None,
+                       workspace: Optional[torch.Tensor] = None):
+    """(row_ptr int32 [R+1], col_idx int32, order int32 [R]).
+
+    With trim (the default) the stream is synchronised once to cut col_idx to
+    its nnz entries; trim=False keeps the full B*H*nB*nB capacity and does not
+    synchronise.  ``out`` may pass preallocated (row_ptr, col_idx, order).
     """
     B, H, nb, _ = mask.shape
     R = B * H * nb
     s = Shape(B, H, nb * 64, 64, 64)
     dev = mask.device
-    row_ptr = torch.empty(R + 1, dtype=torch.int32, device=dev)
-    col_idx = torch.empty(max(R * nb, 1), dtype=torch.int32, device=dev)
-    order = torch.empty(R, dtype=torch.int32, device=dev)
+    if not mask.is_contiguous() or mask.dtype != torch.uint8:
+        raise ValueError("mask must be contiguous uint8 [B, H, nB, nB]")
+    if out is None:
+        out = (torch.empty(R + 1, dtype=torch.int32, device=dev),
+               torch.empty(max(R * nb, 1), dtype=torch.int32, device=dev),
+               torch.empty(R, dtype=torch.int32, device=dev))
+    row_ptr, col_idx, order = out
+    if row_ptr.numel() < R + 1 or col_idx.numel() < R * nb or order.numel() < R:
+        raise ValueError("out tensors too small")
     L = lib()
-    ws = _workspace(L.carnator_compact_block_mask_workspace_size(ctypes.byref(s)), dev)
-    _check(L.carnator_compact_block_mask(_ptr(mask.contiguous()), ctypes.byref(s), _ptr(row_ptr),
-                                         _ptr(col_idx), _ptr(order), _ptr(ws), ws.numel(), _stream(mask)))
-    nnz = int(row_ptr[-1].item())
-    return row_ptr, col_idx[:nnz], order
+    if workspace is None:
+        workspace = compact_block_mask_workspace(mask)
+    _check(L.carnator_compact_block_mask(_ptr(mask), ctypes.byref(s), _ptr(row_ptr), _ptr(col_idx), _ptr(order),
+                                         _ptr(workspace), workspace.numel(), _stream(mask)))
+    if trim:
+        nnz = int(row_ptr[-1].item())
+        return row_ptr, col_idx[:nnz], order
+    return row_ptr, col_idx, order
 
 
 def block_sparse_attn_workspace(q: torch.Tensor, block: int) -> torch.Tensor:
@@ -216,6 +237,33 @@ def block_sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, mask: t
                                         out.stride(0), out.stride(1), out.stride(2), ctypes.byref(s),
                                         _ptr(mask), float(scale), _ptr(lse), _ptr(workspace),
                                         workspace.numel(), _stream(q)))
+    return (out, lse) if return_lse else out
+
+
+def block_sparse_attn_lists(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, lists, block: int,
+                            scale: float = 0.0, return_lse: bool = False, out: Optional[torch.Tensor] = None):
+    """block_sparse_attn with the mask given as the (row_ptr, col_idx, order)
+    lists of compact_block_mask (carnator_block_sparse_attn_lists)."""
+    s = _shape(q, block)
+    for t, n in ((k, "k"), (v, "v")):
+        if tuple(t.shape) != tuple(q.shape):
+            raise ValueError("%s shape differs from q" % n)
+    row_ptr, col_idx, order = lists
+    nb = -(-s.seq_len // block)
+    R = s.batch * s.heads * nb
+    for t, n, need in ((row_ptr, "row_ptr", R + 1), (order, "order", R)):
+        if t.dtype != torch.int32 or not t.is_cuda or t.numel() < need:
+            raise ValueError("%s must be int32 on the GPU with at least %d entries" % (n, need))
+    if col_idx.dtype != torch.int32 or not col_idx.is_cuda:
+        raise ValueError("col_idx must be int32 on the GPU")
+    if out is None:
+        out = torch.empty_like(q, memory_format=torch.contiguous_format)
+    lse = torch.empty(s.batch, s.heads, s.seq_len, dtype=torch.float32, device=q.device) if return_lse else None
+    qv, kv, vv = _view(q), _view(k), _view(v)
+    _check(lib().carnator_block_sparse_attn_lists(ctypes.byref(qv), ctypes.byref(kv), ctypes.byref(vv), _ptr(out),
+                                                  out.stride(0), out.stride(1), out.stride(2), ctypes.byref(s),
+                                                  _ptr(row_ptr), _ptr(col_idx), _ptr(order), float(scale),
+                                                  _ptr(lse), _stream(q)))
     return (out, lse) if return_lse else out
 
 

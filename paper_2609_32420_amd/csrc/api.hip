@@ -239,6 +239,31 @@ int carnator_block_sparse_attn(const carnator_view *q, const carnator_view *k,
   return ok();
 }
 
+int carnator_block_sparse_attn_lists(const carnator_view *q, const carnator_view *k,
+                                     const carnator_view *v, void *out, int64_t osb, int64_t osh,
+                                     int64_t osn, const carnator_shape *s, const int32_t *row_ptr,
+                                     const int32_t *col_idx, const int32_t *order, float scale,
+                                     float *lse, hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if ((rc = check_view(q, s, "q"))) return rc;
+  if ((rc = check_view(k, s, "k"))) return rc;
+  if ((rc = check_view(v, s, "v"))) return rc;
+  if (!out) return fail(CARNATOR_E_NULL, "out is NULL");
+  if (!row_ptr || !col_idx || !order) return fail(CARNATOR_E_NULL, "row_ptr, col_idx and order must be non-NULL");
+  if (reinterpret_cast<uintptr_t>(out) % 16 != 0)
+    return fail(CARNATOR_E_ALIGN, "out must be 16-byte aligned");
+  if (osb % 8 || osh % 8 || osn % 8) return fail(CARNATOR_E_ALIGN, "out strides must be multiples of 8");
+  if (osn < s->head_dim || osb < 0 || osh < 0) return fail(CARNATOR_E_SHAPE, "out strides out of range");
+  if (!isfinite(scale)) return fail(CARNATOR_E_SHAPE, "scale must be finite");
+  const float sc = scale > 0.f ? scale : (float)(1.0 / sqrt((double)s->head_dim));
+  hipError_t e = launch_bsattn(to_view(q), to_view(k), to_view(v), static_cast<uint16_t *>(out), osb, osh,
+                               osn, s->batch, s->heads, s->seq_len, s->head_dim, s->block, row_ptr,
+                               col_idx, order, sc, lse, stream);
+  if (e != hipSuccess) return hip_fail(e, "bsattn");
+  return ok();
+}
+
 // ---------------------------------------------------------------- signature scan
 
 size_t carnator_signature_sim_workspace_size(int64_t nq, int64_t m, int32_t topk) {

@@ -142,11 +142,15 @@ bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, i
   constexpr int KT = C::KT, MT = C::MT;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
 
-  const int row = order[blockIdx.x];
+  // rows, list extents and block indices are clamped into range, so that
+  // malformed lists cannot reach outside the tensors
+  const int R = (int)gridDim.x;
+  const int row = min(max(order[blockIdx.x], 0), R - 1);
   const int bh = row / nB;
   const int qb = row - bh * nB;
   const int b = bh / H, h = bh - b * H;
-  const int e0 = row_ptr[row], e1 = row_ptr[row + 1];
+  const int Lr = min(max(row_ptr[row + 1] - row_ptr[row], 0), nB);
+  const int e0 = min(max(row_ptr[row], 0), R * nB - Lr), e1 = e0 + Lr;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
@@ -411,14 +415,14 @@ bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, i
     int *list = reinterpret_cast<int *>(lds + C::LIST);
     // prologue: K(0), K(1) (both halves of block 0), the row's list into LDS;
     // S(0)
-    int blk0 = col_idx[e0];
-    int blk1 = L > 1 ? col_idx[e0 + 1] : 0;
+    int blk0 = min(max(col_idx[e0], 0), nB - 1);
+    int blk1 = L > 1 ? min(max(col_idx[e0 + 1], 0), nB - 1) : 0;
     {
       const int k0 = blk0 * BS;
       issue_tile(tile_base(kbase, k.sn, min(k0, kmax)), koff, wdst);
       issue_tile(tile_base(kbase, k.sn, min(k0 + KT, kmax)), koff, wdst + C::TB);
     }
-    for (int i = threadIdx.x; i < L; i += C::NT) list[i] = col_idx[e0 + i];
+    for (int i = threadIdx.x; i < L; i += C::NT) list[i] = min(max(col_idx[e0 + i], 0), nB - 1);
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     qk_plain(sc);
     if (blk0 * BS + KT > N) mask_tail(sc, blk0 * BS);

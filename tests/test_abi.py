@@ -125,6 +125,24 @@ def test_attention_rejects_bad_arguments(L):
     assert call(scale=float("inf")) == -2
 
 
+def test_attention_lists_rejects_bad_arguments(L):
+    s = _shape()
+    q = _view()
+    out = ctypes.c_void_p(0x20000)
+    p = ctypes.c_void_p(0x30000)
+
+    def call(o=out, osn=64, rp=p, ci=p, od=p, qv=q, scale=0.0, shape=s):
+        return L.carnator_block_sparse_attn_lists(ctypes.byref(qv), ctypes.byref(q), ctypes.byref(q), o, 0, 0, osn,
+                                                  ctypes.byref(shape), rp, ci, od, scale, None, None)
+    assert call(o=None) == -1
+    assert call(rp=None) == -1 and call(ci=None) == -1 and call(od=None) == -1
+    assert call(o=ctypes.c_void_p(0x20002)) == -4
+    assert call(osn=12) == -4
+    assert call(scale=float("nan")) == -2
+    assert call(shape=_shape(d=96)) == -3
+    assert "NULL" in _err(L) or _err(L)
+
+
 def test_merge_compact_signature_reject(L):
     s = _shape()
     assert L.carnator_merge_target_rows(None, ctypes.byref(s), ctypes.c_void_p(0x100), None, None) == -1

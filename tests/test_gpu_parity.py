@@ -226,6 +226,22 @@ def test_end_to_end_path(wid):
     _compare_rows(o, ro, None, None, [r for r in rows if r[1] < 2], wl.seq_len, wl.block)
 
 
+@pytest.mark.parametrize("wid", [0, 1])
+def test_attention_from_lists_matches_mask_call(wid):
+    """carnator_block_sparse_attn_lists on the lists of carnator_compact_block_mask
+    runs the same kernel as carnator_block_sparse_attn: bit-identical O and LSE."""
+    wl, x = _inputs(wid)
+    mask = P.build_block_mask(x["q_hist"], x["k_hist"], wl.block, wl.tau)
+    P.merge_target_rows(mask, x["row_flags"], x["col_flags"])
+    o1, l1 = P.block_sparse_attn(x["q"], x["k"], x["v"], mask, wl.block, return_lse=True)
+    lists = P.compact_block_mask(mask, trim=False)
+    o2, l2 = P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists, wl.block, return_lse=True)
+    o3 = P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists, wl.block)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(o1, o3)
+    assert torch.equal(l1, l2)
+
+
 @pytest.mark.parametrize("N,bs,d", [(50, 64, 64), (64, 64, 128), (200, 128, 64), (333, 64, 128),
                                     (1000, 128, 128), (2048, 64, 64)])
 def test_attention_ragged_shapes_and_dims(N, bs, d):
