@@ -80,68 +80,86 @@ __global__ void __launch_bounds__(256) pool_kernel(View q, View k, int H, int N,
   }
 }
 
-// Descending logit, lower block index first on equality.
-__device__ inline bool before(double sa, int ja, double sb, int jb) {
-  return sa > sb || (sa == sb && ja < jb);
+// ---- selection --------------------------------------------------------------
+//
+// Sort keys: an order-preserving map of the fp64 logit onto uint64 whose low
+// 11 bits are replaced by (2047 - block index).  Sorting the keys in
+// descending order is sorting by logit with the lower index first among
+// logits equal in their top 53 bits; logits closer than that (2^-42
+// relative) lie deep inside the 1e-6 tie band, where the final choice is made
+// by block index anyway.  The exact logit of each sorted entry is read back
+// by its index.
+__device__ inline uint64_t sel_key(double s, int j) {
+  const uint64_t b = (uint64_t)__double_as_longlong(s);
+  const uint64_t m = (b >> 63) ? ~b : (b | 0x8000000000000000ull);
+  return (m & ~0x7ffull) | (uint64_t)(2047 - j);
+}
+__device__ inline int sel_index(uint64_t k) { return 2047 - (int)(k & 0x7ff); }
+
+// Lane exchange with lane ^ o (o a power of two below 64) without LDS
+// round trips: DPP quad permutes for 1 and 2, ds_swizzle for 4 and 8,
+// v_permlane16/32_swap for 16 and 32.
+template <int O>
+__device__ inline uint32_t xchg32(uint32_t x, int lane) {
+  if constexpr (O == 1) return __builtin_amdgcn_update_dpp(0u, x, 0xB1, 0xF, 0xF, false);
+  else if constexpr (O == 2) return __builtin_amdgcn_update_dpp(0u, x, 0x4E, 0xF, 0xF, false);
+  else if constexpr (O == 4 || O == 8) return __builtin_amdgcn_ds_swizzle(x, (O << 10) | 0x1f);
+  else if constexpr (O == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    return (lane & 16) ? r[0] : r[1];
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return (lane & 32) ? r[0] : r[1];
+  }
+}
+template <int O>
+__device__ inline uint64_t xchg64(uint64_t x, int lane) {
+  const uint32_t lo = xchg32<O>((uint32_t)x, lane);
+  const uint32_t hi = xchg32<O>((uint32_t)(x >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
 }
 
-// One in-register compare-exchange stage (pair distance ST < E elements).
+// One compare-exchange stage of a descending bitonic sort of P = 64 E keys
+// held lane-major (lane L holds positions L E .. L E + E - 1).
 template <int E, int ST>
-__device__ inline void bitonic_inreg(double (&s)[E], int (&j)[E], int lane, int size) {
+__device__ inline void bitonic_stage(uint64_t (&k)[E], int lane, int size) {
+  if constexpr (ST < E) {
 #pragma unroll
-  for (int u = 0; u < E; ++u) {
-    if ((u & ST) == 0) {
-      const int u2 = u | ST;
-      const int p = lane * E + u;
-      const bool dir = (p & size) == 0;
-      const bool sw = dir ? before(s[u2], j[u2], s[u], j[u]) : before(s[u], j[u], s[u2], j[u2]);
-      if (sw) {
-        const double ts = s[u];
-        s[u] = s[u2];
-        s[u2] = ts;
-        const int tj = j[u];
-        j[u] = j[u2];
-        j[u2] = tj;
+    for (int u = 0; u < E; ++u) {
+      if ((u & ST) == 0) {
+        const int u2 = u | ST;
+        const int p = lane * E + u;
+        const bool desc = (p & size) == 0;  // this run sorts descending
+        const uint64_t a = k[u], c = k[u2];
+        const bool sw = desc ? (c > a) : (a > c);
+        k[u] = sw ? c : a;
+        k[u2] = sw ? a : c;
       }
+    }
+  } else {
+    constexpr int LX = ST / E;
+#pragma unroll
+    for (int u = 0; u < E; ++u) {
+      const int p = lane * E + u;
+      const uint64_t o = xchg64<LX>(k[u], lane);
+      const bool desc = (p & size) == 0;
+      const bool lower = (p & ST) == 0;
+      // the lower position of a pair keeps the larger key in a descending run
+      const bool keep_big = lower == desc;
+      const uint64_t a = k[u];
+      k[u] = keep_big ? (a > o ? a : o) : (a < o ? a : o);
     }
   }
 }
-
-// Wave-level bitonic sort of P = 64*E (score, index) pairs held lane-major:
-// lane L holds sorted positions L*E .. L*E+E-1.  Pairs closer than E
-// positions are exchanged inside a lane, farther pairs across lanes.
-template <int E>
-__device__ inline void wave_bitonic(double (&s)[E], int (&j)[E], int lane) {
-  constexpr int P = 64 * E;
-#pragma unroll 1
-  for (int size = 2; size <= P; size <<= 1) {
-#pragma unroll 1
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      if (stride < E) {
-        if constexpr (E > 1) if (stride == 1) bitonic_inreg<E, 1>(s, j, lane, size);
-        if constexpr (E > 2) if (stride == 2) bitonic_inreg<E, 2>(s, j, lane, size);
-        if constexpr (E > 4) if (stride == 4) bitonic_inreg<E, 4>(s, j, lane, size);
-        if constexpr (E > 8) if (stride == 8) bitonic_inreg<E, 8>(s, j, lane, size);
-        if constexpr (E > 16) if (stride == 16) bitonic_inreg<E, 16>(s, j, lane, size);
-      } else {
-        const int lx = stride / E;
-#pragma unroll
-        for (int u = 0; u < E; ++u) {
-          const int p = lane * E + u;
-          const double os = __shfl_xor(s[u], lx);
-          const int oj = __shfl_xor(j[u], lx);
-          const bool dir = (p & size) == 0;
-          const bool lower = (p & stride) == 0;
-          const bool mine_first = before(s[u], j[u], os, oj);
-          const bool want_first = (lower == dir);
-          if (mine_first != want_first) {
-            s[u] = os;
-            j[u] = oj;
-          }
-        }
-      }
-    }
-  }
+template <int E, int ST>
+__device__ inline void bitonic_merge(uint64_t (&k)[E], int lane, int size) {
+  bitonic_stage<E, ST>(k, lane, size);
+  if constexpr (ST > 1) bitonic_merge<E, ST / 2>(k, lane, size);
+}
+template <int E, int SIZE>
+__device__ inline void bitonic_sort(uint64_t (&k)[E], int lane) {
+  if constexpr (SIZE > 2) bitonic_sort<E, SIZE / 2>(k, lane);
+  bitonic_merge<E, SIZE / 2>(k, lane, SIZE);
 }
 
 __device__ inline double wave_sum(double x) {
@@ -150,70 +168,78 @@ __device__ inline double wave_sum(double x) {
   return x;
 }
 
-// One workgroup of 8 waves per (bh, R = 8 consecutive query blocks).
-// Phase 1 computes the R x nB pooled logits into LDS; phase 2 gives each wave
-// one row to select.
-constexpr int kSelThreads = 512;
+// One workgroup of R waves per (bh, R consecutive query blocks).
+//
+// Phase 1, s_ij = sigma <qbar_i, kbar_j>: the R pooled query rows sit in LDS;
+// a wave takes 16 key blocks at a time and forms the 16 x 16 tile of dot
+// products on the fp64 matrix cores (16x16x4 steps over the channels, kbar^T
+// read as 128-byte runs).  With R = 8 the upper half of the tile repeats row
+// R - 1 and is not stored.  Phase 2 gives each wave one row.
 template <int D, int E, int R>
-__global__ void __launch_bounds__(kSelThreads) select_kernel(const double *__restrict__ qbar,
-                                                             const double *__restrict__ kbarT, int nB,
-                                                             double sigma, double tau,
-                                                             uint8_t *__restrict__ mask) {
-  static_assert(R == 8, "one row per wave");
+__global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict__ qbar,
+                                                        const double *__restrict__ kbarT, int nB,
+                                                        double sigma, double tau,
+                                                        uint8_t *__restrict__ mask) {
   extern __shared__ double sc[];  // [R][nB] logits, then [R][D] pooled queries
   const int bh = blockIdx.y;
   const int r0 = blockIdx.x * R;
   const int nr = min(R, nB - r0);
   const double *qb = qbar + ((int64_t)bh * nB + r0) * D;
   const double *kt = kbarT + (int64_t)bh * D * nB;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
 
-  // ---- phase 1: s_ij = sigma * <qbar_i, kbar_j>.  The R pooled query rows
-  // sit in LDS; thread t owns rows 4 (t / 256) .. +4 of key blocks
-  // t % 256 + 256 u, and streams kbar^T[c][j] (coalesced across lanes) 16
-  // channels at a time so the loads overlap.
   double *qs = sc + R * nB;
-  for (int x = threadIdx.x; x < R * D; x += kSelThreads) {
+  for (int x = threadIdx.x; x < R * D; x += 64 * R) {
     const int r = x / D;
     qs[x] = qb[min(r, nr - 1) * D + (x - r * D)];
   }
   __syncthreads();
-  const int rg = (threadIdx.x >> 8) * 4;
-  for (int jj = threadIdx.x & 255; jj < nB; jj += 256) {
-    double acc[4] = {0.0, 0.0, 0.0, 0.0};
-    for (int c0 = 0; c0 < D; c0 += 16) {
-      double kv[16];
+  {
+    // fp64 MFMA 16x16x4: wave w owns key blocks 16 w .. 16 w + 15 (then
+    // + 16 R ...); lane l supplies qbar[row l % 16][4 c + l / 16] and
+    // kbar[key l % 16][4 c + l / 16] and receives S[l / 16 + 4 v][l % 16].
+    const int li = lane & 15, lk = lane >> 4;
+    for (int j0 = wave * 16; j0 < nB; j0 += 16 * R) {
+      const int jc = min(j0 + li, nB - 1);
+      typedef double f64x4 __attribute__((ext_vector_type(4)));
+      f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+      const double *kc = kt + (int64_t)lk * nB + jc;
+      const double *qr = qs + min(li, R - 1) * D + lk;
 #pragma unroll
-      for (int u = 0; u < 16; ++u) kv[u] = kt[(int64_t)(c0 + u) * nB + jj];
+      for (int c0 = 0; c0 < D / 4; c0 += 8) {
+        double kv[8];
 #pragma unroll
-      for (int u = 0; u < 16; u += 2)
+        for (int u = 0; u < 8; ++u) kv[u] = kc[(int64_t)(4 * (c0 + u)) * nB];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const double2 qv = *reinterpret_cast<const double2 *>(qs + (rg + r) * D + c0 + u);
-          acc[r] = fma(qv.x, kv[u], acc[r]);
-          acc[r] = fma(qv.y, kv[u + 1], acc[r]);
+        for (int u = 0; u < 8; ++u) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[4 * (c0 + u)], kv[u], acc, 0, 0, 0);
+      }
+      const int j = j0 + li;
+      if (j < nB) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int r = lk + 4 * v;
+          if (r < nr) sc[r * nB + j] = sigma * acc[v];
         }
+      }
     }
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (rg + r < nr) sc[(rg + r) * nB + jj] = sigma * acc[r];
   }
   __syncthreads();
 
   // ---- phase 2: selection, one row per wave
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  for (int r = wave; r < nr; r += kSelThreads / 64) {
+  for (int r = wave; r < nr; r += R) {
     const double *row = sc + r * nB;
     uint8_t *out = mask + ((int64_t)bh * nB + r0 + r) * nB;
-    double s[E];
-    int j[E];
+    uint64_t key[E];
 #pragma unroll
     for (int u = 0; u < E; ++u) {
       const int p = lane * E + u;
-      j[u] = p;
-      s[u] = p < nB ? row[p] : -INFINITY;
+      key[u] = p < nB ? sel_key(row[p], p) : 0ull;  // 0 sorts last
     }
-    wave_bitonic<E>(s, j, lane);
+    bitonic_sort<E, 64 * E>(key, lane);
+    double s[E];
+#pragma unroll
+    for (int u = 0; u < E; ++u) s[u] = lane * E + u < nB ? row[sel_index(key[u])] : -INFINITY;
 
     // softmax over the sorted row; positions >= nB carry -inf and weigh 0
     const double smax = __shfl(s[0], 0);
@@ -312,39 +338,37 @@ static hipError_t launch_select_dr(const double *qbar, const double *kbarT, int 
   dim3 grid((nB + R - 1) / R, BH);
   const size_t lds = (size_t)R * (nB + D) * sizeof(double);
   const int P = nB <= 64 ? 64 : (1 << (32 - __builtin_clz((unsigned)(nB - 1))));
-#define CARNATOR_LDS_ATTR(EE)                                                                     \
+#define CARNATOR_SEL(EE)                                                                          \
   do {                                                                                            \
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&select_kernel<D, EE, R>),  \
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);     \
     if (e != hipSuccess) return e;                                                                \
+    hipLaunchKernelGGL((select_kernel<D, EE, R>), grid, dim3(64 * R), lds, s, qbar, kbarT, nB,    \
+                       sigma, tau, mask);                                                         \
   } while (0)
   switch (P / 64) {
-    case 1: CARNATOR_LDS_ATTR(1); break;
-    case 2: CARNATOR_LDS_ATTR(2); break;
-    case 4: CARNATOR_LDS_ATTR(4); break;
-    case 8: CARNATOR_LDS_ATTR(8); break;
-    case 16: CARNATOR_LDS_ATTR(16); break;
-    case 32: CARNATOR_LDS_ATTR(32); break;
+    case 1: CARNATOR_SEL(1); break;
+    case 2: CARNATOR_SEL(2); break;
+    case 4: CARNATOR_SEL(4); break;
+    case 8: CARNATOR_SEL(8); break;
+    case 16: CARNATOR_SEL(16); break;
+    case 32:
+      if constexpr (R <= 8) CARNATOR_SEL(32);
+      else return hipErrorInvalidValue;
+      break;
     default: return hipErrorInvalidValue;
   }
-#undef CARNATOR_LDS_ATTR
-  switch (P / 64) {
-    case 1: hipLaunchKernelGGL((select_kernel<D, 1, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    case 2: hipLaunchKernelGGL((select_kernel<D, 2, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    case 4: hipLaunchKernelGGL((select_kernel<D, 4, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    case 8: hipLaunchKernelGGL((select_kernel<D, 8, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    case 16: hipLaunchKernelGGL((select_kernel<D, 16, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    case 32: hipLaunchKernelGGL((select_kernel<D, 32, R>), grid, dim3(kSelThreads), lds, s, qbar, kbarT, nB, sigma, tau, mask); break;
-    default: return hipErrorInvalidValue;
-  }
+#undef CARNATOR_SEL
   return hipGetLastError();
 }
 
-// 8 query blocks per workgroup: their logits and pooled rows take
-// 64 * (nB + d) bytes of LDS (at most 139 KiB for nB = 2048, d = 128).
+// R query blocks per workgroup (one wave each): their logits and pooled rows
+// take 8 R (nB + d) bytes of LDS, which stays within 160 KiB with R = 16 up
+// to nB = 1024 and with R = 8 up to nB = 2048.
 template <int D>
 static hipError_t launch_select_d(const double *qbar, const double *kbarT, int BH, int nB,
                                   double sigma, double tau, uint8_t *mask, hipStream_t s) {
+  if (nB <= 1024) return launch_select_dr<D, 16>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
   return launch_select_dr<D, 8>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
 }
 
