@@ -95,15 +95,26 @@ __device__ inline uint64_t sel_key(double s, int j) {
   return (m & ~0x7ffull) | (uint64_t)(2047 - j);
 }
 __device__ inline int sel_index(uint64_t k) { return 2047 - (int)(k & 0x7ff); }
+// The logit a sort key stands for, up to its low 11 bits (used only to pick
+// bisection points).
+__device__ inline double key_value(uint64_t k) {
+  const uint64_t b = (k >> 63) ? (k & 0x7fffffffffffffffull) : ~k;
+  return __longlong_as_double((long long)b);
+}
 
-// Lane exchange with lane ^ o (o a power of two below 64) without LDS
-// round trips: DPP quad permutes for 1 and 2, ds_swizzle for 4 and 8,
-// v_permlane16/32_swap for 16 and 32.
+// Cross-lane partner values for wave-wide reductions without LDS round
+// trips: quad permutes (lane ^ 1, lane ^ 2), the half-row and row mirrors
+// (lane 7 - i and 15 - i within 8 and 16 lanes) and the 16- and 32-lane
+// swaps.  After the steps below 2^s every lane of a 2^s-lane group holds the
+// group's value, so the mirrors pair each group with its sibling, and every
+// lane ends with the same result (each step combines the same two operands
+// in every lane; + and max are commutative).
 template <int O>
-__device__ inline uint32_t xchg32(uint32_t x, int lane) {
+__device__ inline uint32_t partner32(uint32_t x, int lane) {
   if constexpr (O == 1) return __builtin_amdgcn_update_dpp(0u, x, 0xB1, 0xF, 0xF, false);
   else if constexpr (O == 2) return __builtin_amdgcn_update_dpp(0u, x, 0x4E, 0xF, 0xF, false);
-  else if constexpr (O == 4 || O == 8) return __builtin_amdgcn_ds_swizzle(x, (O << 10) | 0x1f);
+  else if constexpr (O == 4) return __builtin_amdgcn_update_dpp(0u, x, 0x141, 0xF, 0xF, false);
+  else if constexpr (O == 8) return __builtin_amdgcn_update_dpp(0u, x, 0x140, 0xF, 0xF, false);
   else if constexpr (O == 16) {
     const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
     return (lane & 16) ? r[0] : r[1];
@@ -113,59 +124,45 @@ __device__ inline uint32_t xchg32(uint32_t x, int lane) {
   }
 }
 template <int O>
-__device__ inline uint64_t xchg64(uint64_t x, int lane) {
-  const uint32_t lo = xchg32<O>((uint32_t)x, lane);
-  const uint32_t hi = xchg32<O>((uint32_t)(x >> 32), lane);
+__device__ inline uint64_t partner64(uint64_t x, int lane) {
+  const uint32_t lo = partner32<O>((uint32_t)x, lane);
+  const uint32_t hi = partner32<O>((uint32_t)(x >> 32), lane);
   return ((uint64_t)hi << 32) | lo;
 }
-
-// One compare-exchange stage of a descending bitonic sort of P = 64 E keys
-// held lane-major (lane L holds positions L E .. L E + E - 1).
-template <int E, int ST>
-__device__ inline void bitonic_stage(uint64_t (&k)[E], int lane, int size) {
-  if constexpr (ST < E) {
-#pragma unroll
-    for (int u = 0; u < E; ++u) {
-      if ((u & ST) == 0) {
-        const int u2 = u | ST;
-        const int p = lane * E + u;
-        const bool desc = (p & size) == 0;  // this run sorts descending
-        const uint64_t a = k[u], c = k[u2];
-        const bool sw = desc ? (c > a) : (a > c);
-        k[u] = sw ? c : a;
-        k[u2] = sw ? a : c;
-      }
-    }
+template <int O>
+__device__ inline double partner_f64(double x, int lane) {
+  return __longlong_as_double((long long)partner64<O>((uint64_t)__double_as_longlong(x), lane));
+}
+template <typename T, typename F>
+__device__ inline T wave_reduce(T x, int lane, F op) {
+  if constexpr (sizeof(T) == 8 && !__is_same(T, double)) {
+    x = op(x, partner64<1>(x, lane));
+    x = op(x, partner64<2>(x, lane));
+    x = op(x, partner64<4>(x, lane));
+    x = op(x, partner64<8>(x, lane));
+    x = op(x, partner64<16>(x, lane));
+    x = op(x, partner64<32>(x, lane));
   } else {
-    constexpr int LX = ST / E;
-#pragma unroll
-    for (int u = 0; u < E; ++u) {
-      const int p = lane * E + u;
-      const uint64_t o = xchg64<LX>(k[u], lane);
-      const bool desc = (p & size) == 0;
-      const bool lower = (p & ST) == 0;
-      // the lower position of a pair keeps the larger key in a descending run
-      const bool keep_big = lower == desc;
-      const uint64_t a = k[u];
-      k[u] = keep_big ? (a > o ? a : o) : (a < o ? a : o);
-    }
+    x = op(x, partner_f64<1>(x, lane));
+    x = op(x, partner_f64<2>(x, lane));
+    x = op(x, partner_f64<4>(x, lane));
+    x = op(x, partner_f64<8>(x, lane));
+    x = op(x, partner_f64<16>(x, lane));
+    x = op(x, partner_f64<32>(x, lane));
   }
-}
-template <int E, int ST>
-__device__ inline void bitonic_merge(uint64_t (&k)[E], int lane, int size) {
-  bitonic_stage<E, ST>(k, lane, size);
-  if constexpr (ST > 1) bitonic_merge<E, ST / 2>(k, lane, size);
-}
-template <int E, int SIZE>
-__device__ inline void bitonic_sort(uint64_t (&k)[E], int lane) {
-  if constexpr (SIZE > 2) bitonic_sort<E, SIZE / 2>(k, lane);
-  bitonic_merge<E, SIZE / 2>(k, lane, SIZE);
-}
-
-__device__ inline double wave_sum(double x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
   return x;
+}
+__device__ inline double wave_sum(double x, int lane) {
+  return wave_reduce(x, lane, [](double a, double b) { return a + b; });
+}
+__device__ inline double wave_max(double x, int lane) {
+  return wave_reduce(x, lane, [](double a, double b) { return fmax(a, b); });
+}
+__device__ inline uint64_t wave_min_u64(uint64_t x, int lane) {
+  return wave_reduce(x, lane, [](uint64_t a, uint64_t b) { return b < a ? b : a; });
+}
+__device__ inline uint64_t wave_max_u64(uint64_t x, int lane) {
+  return wave_reduce(x, lane, [](uint64_t a, uint64_t b) { return b > a ? b : a; });
 }
 
 // One workgroup of R waves per (bh, R consecutive query blocks).
@@ -174,15 +171,25 @@ __device__ inline double wave_sum(double x) {
 // a wave takes 16 key blocks at a time and forms the 16 x 16 tile of dot
 // products on the fp64 matrix cores (16x16x4 steps over the channels, kbar^T
 // read as 128-byte runs).  With R = 8 the upper half of the tile repeats row
-// R - 1 and is not stored.  Phase 2 gives each wave one row.
+// R - 1 and is not stored.  Phase 2 gives each wave one row (E = positions
+// per lane, 64 E >= nB).
 template <int D, int E, int R>
 __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict__ qbar,
                                                         const double *__restrict__ kbarT, int nB,
                                                         double sigma, double tau,
-                                                        uint8_t *__restrict__ mask) {
+                                                        uint8_t *__restrict__ mask, int BH) {
   extern __shared__ double sc[];  // [R][nB] logits, then [R][D] pooled queries
-  const int bh = blockIdx.y;
-  const int r0 = blockIdx.x * R;
+  // Workgroups are dealt to the 8 XCDs in turn.  Logical workgroup
+  // (L mod 8) ceil(G / 8) + L / 8 gives each XCD a contiguous run of
+  // (head, row block) pairs, so an XCD's L2 fetches the kbar^T of about
+  // BH / 8 heads instead of all of them.
+  const int nbx = (nB + R - 1) / R;
+  const int G = nbx * BH;
+  const int per = (G + 7) / 8;
+  const int T = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (T >= G) return;  // the whole workgroup, before any barrier
+  const int bh = T / nbx;
+  const int r0 = (T - bh * nbx) * R;
   const int nr = min(R, nB - r0);
   const double *qb = qbar + ((int64_t)bh * nB + r0) * D;
   const double *kt = kbarT + (int64_t)bh * D * nB;
@@ -206,13 +213,18 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
       f64x4 acc = {0.0, 0.0, 0.0, 0.0};
       const double *kc = kt + (int64_t)lk * nB + jc;
       const double *qr = qs + min(li, R - 1) * D + lk;
+      // The channel steps start at a different place in every wave: walking
+      // them in lockstep sends every wave of the chip to the same few L2
+      // channels at once (the heads' kbar^T sit a power-of-two apart).
+      const int rot = (wave * 5 + T * 3) & (D / 4 - 1);
 #pragma unroll
       for (int c0 = 0; c0 < D / 4; c0 += 8) {
         double kv[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) kv[u] = kc[(int64_t)(4 * (c0 + u)) * nB];
+        for (int u = 0; u < 8; ++u) kv[u] = kc[(int64_t)(4 * ((c0 + u + rot) & (D / 4 - 1))) * nB];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[4 * (c0 + u)], kv[u], acc, 0, 0, 0);
+        for (int u = 0; u < 8; ++u)
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[4 * ((c0 + u + rot) & (D / 4 - 1))], kv[u], acc, 0, 0, 0);
       }
       const int j = j0 + li;
       if (j < nB) {
@@ -226,89 +238,129 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
   }
   __syncthreads();
 
-  // ---- phase 2: selection, one row per wave
+  // ---- phase 2: selection, one row per wave.  Lane l holds positions
+  // u 64 + l.  The k-th largest sort key K* (k the shortest prefix whose
+  // mass reaches tau) is found by bisection over the keys, keeping
+  // mass(key >= lo) >= tau > mass(key >= hi) until [lo, hi) holds one key.
   for (int r = wave; r < nr; r += R) {
     const double *row = sc + r * nB;
     uint8_t *out = mask + ((int64_t)bh * nB + r0 + r) * nB;
+    double pl[E];
     uint64_t key[E];
+    double smax = -INFINITY;
+    uint64_t kmin = ~0ull, kmax = 0ull;
 #pragma unroll
     for (int u = 0; u < E; ++u) {
-      const int p = lane * E + u;
-      key[u] = p < nB ? sel_key(row[p], p) : 0ull;  // 0 sorts last
+      const int p = u * 64 + lane;
+      const bool ok = p < nB;
+      pl[u] = ok ? row[p] : -INFINITY;  // the logit until the softmax below
+      key[u] = ok ? sel_key(pl[u], p) : 0ull;  // valid keys are > 2047
+      smax = fmax(smax, pl[u]);
+      if (ok) {
+        kmin = key[u] < kmin ? key[u] : kmin;
+        kmax = key[u] > kmax ? key[u] : kmax;
+      }
     }
-    bitonic_sort<E, 64 * E>(key, lane);
-    double s[E];
-#pragma unroll
-    for (int u = 0; u < E; ++u) s[u] = lane * E + u < nB ? row[sel_index(key[u])] : -INFINITY;
-
-    // softmax over the sorted row; positions >= nB carry -inf and weigh 0
-    const double smax = __shfl(s[0], 0);
-    double e[E];
+    smax = wave_max(smax, lane);
+    kmin = wave_min_u64(kmin, lane);
+    kmax = wave_max_u64(kmax, lane);
+    // softmax p = exp(s - max) / sum
     double lsum = 0.0;
 #pragma unroll
     for (int u = 0; u < E; ++u) {
-      e[u] = (lane * E + u < nB) ? exp(s[u] - smax) : 0.0;
-      lsum += e[u];
+      pl[u] = (u * 64 + lane < nB) ? exp(pl[u] - smax) : 0.0;
+      lsum += pl[u];
     }
-    const double Z = wave_sum(lsum);
-    // inclusive prefix of p = e / Z in sorted order
-    double pl[E];
-    double run = 0.0;
+    const double Z = wave_sum(lsum, lane);
 #pragma unroll
-    for (int u = 0; u < E; ++u) {
-      pl[u] = e[u] / Z;
-      run += pl[u];
-    }
-    double incl = run;  // inclusive scan of the lane totals
+    for (int u = 0; u < E; ++u) pl[u] = pl[u] / Z;
+
+    // mass and count of the keys >= K (identical in every lane)
+    auto mass_ge = [&](uint64_t K, int &cnt) __attribute__((always_inline)) {
+      double m = 0.0;
+      int c = 0;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const double y = __shfl_up(incl, o);
-      if (lane >= o) incl += y;
-    }
-    double excl = __shfl_up(incl, 1);
-    if (lane == 0) excl = 0.0;
-    int first = E;
-    double cum = excl;
-#pragma unroll
-    for (int u = 0; u < E; ++u) {
-      cum += pl[u];
-      if (first == E && lane * E + u < nB && cum >= tau) first = u;
-    }
-    const unsigned long long hit = __ballot(first < E);
-    int k;
-    if (hit) {
-      const int hl = __ffsll((long long)hit) - 1;
-      k = hl * E + __shfl(first, hl) + 1;
+      for (int u = 0; u < E; ++u) {
+        const bool ge = key[u] >= K;
+        m += ge ? pl[u] : 0.0;
+        c += __popcll(__ballot(ge));
+      }
+      cnt = c;
+      return wave_sum(m, lane);
+    };
+    int cnt_lo, cnt_hi = 0;
+    uint64_t lo = kmin, hi = kmax + 1;
+    uint64_t kstar;
+    if (!(mass_ge(lo, cnt_lo) >= tau)) {
+      kstar = kmin;  // the whole row falls short of tau: keep every block
     } else {
-      k = nB;
-    }
-    // cut score = sorted position k-1
-    const int cl = (k - 1) / E, cu = (k - 1) % E;
-    double mine = 0.0;
+      // Split at the midpoint of the values while that separates keys; once
+      // it does not (a run of equal logits), split at the highest bit in
+      // which the interval's smallest and largest keys differ, which leaves
+      // keys on both sides and resolves equal logits by their index bits.
+      bool trie = false;
+      for (int it = 0; it < 192 && cnt_lo - cnt_hi > 1; ++it) {
+        uint64_t K = 0;
+        if (!trie) {
+          const double lv = key_value(lo), hv = key_value(hi - 1);
+          K = sel_key(lv + 0.5 * (hv - lv), 2047);
+          trie = !(K > lo && K < hi);
+        }
+        if (trie) {
+          uint64_t a = ~0ull, b = 0ull;
 #pragma unroll
-    for (int u = 0; u < E; ++u)
-      if (u == cu) mine = s[u];
-    const double cut = __shfl(mine, cl);
+          for (int u = 0; u < E; ++u) {
+            const bool in = key[u] >= lo && key[u] < hi;
+            a = in && key[u] < a ? key[u] : a;
+            b = in && key[u] > b ? key[u] : b;
+          }
+          a = wave_min_u64(a, lane);
+          b = wave_max_u64(b, lane);
+          // a < b: the interval holds at least two (distinct) keys
+          K = b & ~((1ull << (63 - __clzll((long long)(a ^ b)))) - 1ull);
+        }
+        const int before = cnt_lo - cnt_hi;
+        int c;
+        const bool up = __builtin_amdgcn_readfirstlane((int)(mass_ge(K, c) >= tau)) != 0;
+        if (up) {
+          lo = K;
+          cnt_lo = c;
+        } else {
+          hi = K;
+          cnt_hi = c;
+        }
+        if (cnt_lo - cnt_hi == before) trie = true;
+      }
+      // the largest key in [lo, hi) (the only one, unless the cap was hit)
+      uint64_t kl = 0ull;
+#pragma unroll
+      for (int u = 0; u < E; ++u)
+        if (key[u] >= lo && key[u] < hi && key[u] > kl) kl = key[u];
+      kstar = wave_max_u64(kl, lane);
+    }
+    int k = 0;
+#pragma unroll
+    for (int u = 0; u < E; ++u) k += __popcll(__ballot(key[u] >= kstar));
+    const double cut = row[sel_index(kstar)];
     const double hiT = cut + kTieEps;
 
     // |S+| : blocks strictly above the tie band
     int nplus = 0;
-    for (int base = 0; base < nB; base += 64) {
-      const int jj = base + lane;
-      const bool above = jj < nB && row[jj] > hiT;
-      nplus += __popcll(__ballot(above));
-    }
+#pragma unroll
+    for (int u = 0; u < E; ++u) nplus += __popcll(__ballot(u * 64 + lane < nB && row[min(u * 64 + lane, nB - 1)] > hiT));
     const int need = k - nplus;
     // write the row in index order; the first `need` tied blocks are kept
     int tied_before = 0;
-    for (int base = 0; base < nB; base += 64) {
-      const int jj = base + lane;
-      double sv = jj < nB ? row[jj] : -INFINITY;
-      const bool above = jj < nB && sv > hiT;
-      const bool tie = jj < nB && fabs(sv - cut) <= kTieEps;
+#pragma unroll
+    for (int u = 0; u < E; ++u) {
+      const int jj = u * 64 + lane;
+      const bool ok = jj < nB;
+      const double sv = row[min(jj, nB - 1)];
+      const bool above = ok && sv > hiT;
+      const bool tie = ok && fabs(sv - cut) <= kTieEps;
       const unsigned long long tb = __ballot(tie);
       const int rank = tied_before + __popcll(tb & ((1ull << lane) - 1ull));
-      if (jj < nB) out[jj] = (above || (tie && rank < need)) ? 1 : 0;
+      if (ok) out[jj] = (above || (tie && rank < need)) ? 1 : 0;
       tied_before += __popcll(tb);
     }
   }
@@ -335,7 +387,8 @@ hipError_t launch_pool(View q, View k, int B, int H, int N, int d, int bs, doubl
 template <int D, int R>
 static hipError_t launch_select_dr(const double *qbar, const double *kbarT, int BH, int nB,
                                    double sigma, double tau, uint8_t *mask, hipStream_t s) {
-  dim3 grid((nB + R - 1) / R, BH);
+  const int G = (nB + R - 1) / R * BH;
+  dim3 grid((G + 7) / 8 * 8);
   const size_t lds = (size_t)R * (nB + D) * sizeof(double);
   const int P = nB <= 64 ? 64 : (1 << (32 - __builtin_clz((unsigned)(nB - 1))));
 #define CARNATOR_SEL(EE)                                                                          \
@@ -344,14 +397,17 @@ static hipError_t launch_select_dr(const double *qbar, const double *kbarT, int 
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);     \
     if (e != hipSuccess) return e;                                                                \
     hipLaunchKernelGGL((select_kernel<D, EE, R>), grid, dim3(64 * R), lds, s, qbar, kbarT, nB,    \
-                       sigma, tau, mask);                                                         \
+                       sigma, tau, mask, BH);                                                     \
   } while (0)
   switch (P / 64) {
     case 1: CARNATOR_SEL(1); break;
     case 2: CARNATOR_SEL(2); break;
     case 4: CARNATOR_SEL(4); break;
     case 8: CARNATOR_SEL(8); break;
-    case 16: CARNATOR_SEL(16); break;
+    case 16:
+      if constexpr (R <= 8) CARNATOR_SEL(16);
+      else return hipErrorInvalidValue;
+      break;
     case 32:
       if constexpr (R <= 8) CARNATOR_SEL(32);
       else return hipErrorInvalidValue;
@@ -363,12 +419,13 @@ static hipError_t launch_select_dr(const double *qbar, const double *kbarT, int 
 }
 
 // R query blocks per workgroup (one wave each): their logits and pooled rows
-// take 8 R (nB + d) bytes of LDS, which stays within 160 KiB with R = 16 up
-// to nB = 1024 and with R = 8 up to nB = 2048.
+// take 8 R (nB + d) bytes of LDS, within 160 KiB for R = 8 up to nB = 2048.
+// R = 16 halves the kbar^T re-reads; it is used while a lane's share of a
+// row (E <= 8 positions) leaves the registers for 16 waves per workgroup.
 template <int D>
 static hipError_t launch_select_d(const double *qbar, const double *kbarT, int BH, int nB,
                                   double sigma, double tau, uint8_t *mask, hipStream_t s) {
-  if (nB <= 1024) return launch_select_dr<D, 16>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
+  if (nB <= 512) return launch_select_dr<D, 16>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
   return launch_select_dr<D, 8>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
 }
 

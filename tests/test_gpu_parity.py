@@ -122,7 +122,8 @@ def test_mask_builder_thresholds_and_explicit_scale(tau):
     _assert_masks_equal(got, want, fragile, tau)
 
 
-@pytest.mark.parametrize("N,bs,d", [(50, 64, 64), (1000, 64, 128), (4100, 128, 64), (9000, 64, 64)])
+@pytest.mark.parametrize("N,bs,d", [(50, 64, 64), (1000, 64, 128), (4100, 128, 64), (9000, 64, 64),
+                                   (70000, 64, 64)])
 def test_mask_builder_ragged_random(N, bs, d):
     g = torch.Generator(device=DEV).manual_seed(N)
     qh = torch.randn(2, 3, N, d, generator=g, device=DEV).to(torch.bfloat16)
@@ -134,11 +135,13 @@ def test_mask_builder_ragged_random(N, bs, d):
     _assert_masks_equal(got, want, fragile, 0.8)
 
 
-def test_mask_builder_constant_input_ties():
-    # All pooled logits equal: k = ceil(tau * nB), the lowest blocks.
-    x = torch.ones(1, 1, 640, 64, dtype=torch.bfloat16, device=DEV)
-    got = P.build_block_mask(x, x, 64, 0.45).cpu().numpy()
-    assert (got[0, 0] == np.array([1] * 5 + [0] * 5, dtype=np.uint8)[None, :]).all()
+@pytest.mark.parametrize("nb,tau,k", [(10, 0.45, 5), (300, 0.123, 37), (1100, 0.4537, 500)])
+def test_mask_builder_constant_input_ties(nb, tau, k):
+    # All pooled logits equal: k = ceil(tau * nB) (tau nB not an integer), the
+    # lowest blocks of every row.
+    x = torch.ones(1, 1, nb * 64, 64, dtype=torch.bfloat16, device=DEV)
+    got = P.build_block_mask(x, x, 64, tau).cpu().numpy()
+    assert (got[0, 0] == np.array([1] * k + [0] * (nb - k), dtype=np.uint8)[None, :]).all()
 
 
 # ---------------------------------------------------------------- merge, compaction
