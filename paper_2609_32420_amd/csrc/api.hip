@@ -122,6 +122,7 @@ const char *carnator_last_error(void) { return g_err; }
 
 // ---------------------------------------------------------------- mask builder
 
+// Builder workspace: pooled Q and K rows (fp64 [BH][nB][d] each).
 size_t carnator_build_block_mask_workspace_size(const carnator_shape *s) {
   if (check_shape(s) != CARNATOR_OK) return 0;
   const size_t per = align_up((size_t)s->batch * s->heads * n_blocks(s) * s->head_dim * sizeof(double));
@@ -152,12 +153,12 @@ int carnator_build_block_mask(const carnator_view *q_hist, const carnator_view *
   if ((rc = check_ws(workspace, ws_bytes, need))) return rc;
   const size_t per = need / 2;
   double *qbar = static_cast<double *>(workspace);
-  double *kbarT = reinterpret_cast<double *>(static_cast<char *>(workspace) + per);
+  double *kbar = reinterpret_cast<double *>(static_cast<char *>(workspace) + per);
   const double sigma = scale > 0.f ? (double)scale : 1.0 / sqrt((double)s->head_dim);
   hipError_t e = launch_pool(to_view(q_hist), to_view(k_hist), s->batch, s->heads, s->seq_len,
-                             s->head_dim, s->block, qbar, kbarT, stream);
+                             s->head_dim, s->block, qbar, kbar, stream);
   if (e != hipSuccess) return hip_fail(e, "pool");
-  e = launch_select(qbar, kbarT, BH, nB, s->head_dim, sigma, mass_threshold, mask_out, stream);
+  e = launch_select(qbar, kbar, BH, nB, s->head_dim, sigma, mass_threshold, mask_out, stream);
   if (e != hipSuccess) return hip_fail(e, "select");
   return ok();
 }

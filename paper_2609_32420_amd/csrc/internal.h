@@ -20,12 +20,12 @@ struct View {
 // ---- block mask builder ----------------------------------------------------
 // Pools Q_hist and K_hist per block (fp64 means over valid tokens).
 //   qbar:  fp64 [BH][nB][d]   (row-major)
-//   kbarT: fp64 [BH][d][nB]   (d-major, so consecutive key blocks are adjacent)
+//   kbar:  fp64 [BH][nB][d]
 hipError_t launch_pool(View q, View k, int B, int H, int N, int d, int bs, double *qbar,
-                       double *kbarT, hipStream_t s);
+                       double *kbar, hipStream_t s);
 // Scores, softmax over key blocks, top-mass selection with the tie rule; writes
 // uint8 [BH][nB][nB].
-hipError_t launch_select(const double *qbar, const double *kbarT, int BH, int nB, int d,
+hipError_t launch_select(const double *qbar, const double *kbar, int BH, int nB, int d,
                          double sigma, double tau, uint8_t *mask, hipStream_t s);
 hipError_t launch_fill_ones(uint8_t *p, size_t n, hipStream_t s);
 

@@ -24,7 +24,7 @@ __device__ inline double bf16_to_f64(uint32_t bits16) {
 template <int D>
 __global__ void __launch_bounds__(256) pool_kernel(View q, View k, int H, int N, int bs, int nB,
                                                    double *__restrict__ qbar,
-                                                   double *__restrict__ kbarT) {
+                                                   double *__restrict__ kbar) {
   constexpr int CPR = D / 8;         // 16-byte chunks per token
   constexpr int G = 256 / CPR;       // token groups
   __shared__ double part[4][D];      // one partial per wave
@@ -73,10 +73,7 @@ __global__ void __launch_bounds__(256) pool_kernel(View q, View k, int H, int N,
   for (int ch = threadIdx.x; ch < D; ch += 256) {
     const double s = ((part[0][ch] + part[1][ch]) + part[2][ch]) + part[3][ch];
     const double mean = s / (double)n;
-    if (which == 0)
-      qbar[((int64_t)bh * nB + blk) * D + ch] = mean;
-    else
-      kbarT[((int64_t)bh * D + ch) * nB + blk] = mean;
+    (which ? kbar : qbar)[((int64_t)bh * nB + blk) * D + ch] = mean;
   }
 }
 
@@ -169,19 +166,26 @@ __device__ inline uint64_t wave_max_u64(uint64_t x, int lane) {
 //
 // Phase 1, s_ij = sigma <qbar_i, kbar_j>: the R pooled query rows sit in LDS;
 // a wave takes 16 key blocks at a time and forms the 16 x 16 tile of dot
-// products on the fp64 matrix cores (16x16x4 steps over the channels, kbar^T
-// read as 128-byte runs).  With R = 8 the upper half of the tile repeats row
-// R - 1 and is not stored.  Phase 2 gives each wave one row (E = positions
-// per lane, 64 E >= nB).
+// products on the fp64 matrix cores (16x16x4 steps over the channels).  The
+// contraction visits the channels in an order that suits the loads: in
+// 16-channel group g, lane (i, k) = (lane & 15, lane >> 4) holds channels
+// 16 g + 4 k .. 16 g + 4 k + 3 of key block i (one 32-byte piece of its kbar
+// row) and feeds channel 16 g + 4 k + t to step t, and the query side takes
+// its channels in the same order.  With R = 8 the upper half of the tile
+// repeats row R - 1 and is not stored.  Phase 2 gives each wave one row
+// (E = positions per lane, 64 E >= nB).
 template <int D, int E, int R>
 __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict__ qbar,
-                                                        const double *__restrict__ kbarT, int nB,
+                                                        const double *__restrict__ kbar, int nB,
                                                         double sigma, double tau,
                                                         uint8_t *__restrict__ mask, int BH) {
-  extern __shared__ double sc[];  // [R][nB] logits, then [R][D] pooled queries
+  // LDS: [R][nB] logits, then the R pooled query rows, QS doubles apart (a
+  // 16-byte pad spreads the 16 rows read by one MFMA step over the banks)
+  constexpr int QS = D + 2;
+  extern __shared__ double sc[];
   // Workgroups are dealt to the 8 XCDs in turn.  Logical workgroup
   // (L mod 8) ceil(G / 8) + L / 8 gives each XCD a contiguous run of
-  // (head, row block) pairs, so an XCD's L2 fetches the kbar^T of about
+  // (head, row block) pairs, so an XCD's L2 fetches the kbar of about
   // BH / 8 heads instead of all of them.
   const int nbx = (nB + R - 1) / R;
   const int G = nbx * BH;
@@ -192,39 +196,55 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
   const int r0 = (T - bh * nbx) * R;
   const int nr = min(R, nB - r0);
   const double *qb = qbar + ((int64_t)bh * nB + r0) * D;
-  const double *kt = kbarT + (int64_t)bh * D * nB;
+  const double *kb = kbar + (int64_t)bh * nB * D;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
 
   double *qs = sc + R * nB;
-  for (int x = threadIdx.x; x < R * D; x += 64 * R) {
-    const int r = x / D;
-    qs[x] = qb[min(r, nr - 1) * D + (x - r * D)];
+  {
+    constexpr int SPT = D / 64;  // staged values per thread (both loads in flight)
+    double sv[SPT];
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) {
+      const int x = threadIdx.x + i * 64 * R, r = x / D, c = x - r * D;
+      sv[i] = qb[min(r, nr - 1) * D + c];
+    }
+#pragma unroll
+    for (int i = 0; i < SPT; ++i) {
+      const int x = threadIdx.x + i * 64 * R, r = x / D, c = x - r * D;
+      qs[r * QS + c] = sv[i];
+    }
   }
   __syncthreads();
   {
-    // fp64 MFMA 16x16x4: wave w owns key blocks 16 w .. 16 w + 15 (then
-    // + 16 R ...); lane l supplies qbar[row l % 16][4 c + l / 16] and
-    // kbar[key l % 16][4 c + l / 16] and receives S[l / 16 + 4 v][l % 16].
+    typedef double f64x4 __attribute__((ext_vector_type(4)));
+    constexpr int NG = D / 16;  // 16-channel groups
     const int li = lane & 15, lk = lane >> 4;
+    const double *qr = qs + min(li, R - 1) * QS + 4 * lk;
+    // The groups start at a different place in every wave: walking them in
+    // lockstep sends every wave of the chip to the same few L2 channels.
+    const int rot = (wave * 5 + T * 3) & (NG - 1);
     for (int j0 = wave * 16; j0 < nB; j0 += 16 * R) {
-      const int jc = min(j0 + li, nB - 1);
-      typedef double f64x4 __attribute__((ext_vector_type(4)));
+      const double *kr = kb + (int64_t)min(j0 + li, nB - 1) * D + 4 * lk;
       f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-      const double *kc = kt + (int64_t)lk * nB + jc;
-      const double *qr = qs + min(li, R - 1) * D + lk;
-      // The channel steps start at a different place in every wave: walking
-      // them in lockstep sends every wave of the chip to the same few L2
-      // channels at once (the heads' kbar^T sit a power-of-two apart).
-      const int rot = (wave * 5 + T * 3) & (D / 4 - 1);
+      // All of the tile's loads are issued before the first product: left to
+      // itself the compiler keeps two in flight, and the tile then costs
+      // D / 8 L2 round trips instead of one.
+      double2 kv[NG][2];
 #pragma unroll
-      for (int c0 = 0; c0 < D / 4; c0 += 8) {
-        double kv[8];
+      for (int g = 0; g < NG; ++g) {
+        const int gr = (g + rot) & (NG - 1);
+        kv[g][0] = *reinterpret_cast<const double2 *>(kr + 16 * gr);
+        kv[g][1] = *reinterpret_cast<const double2 *>(kr + 16 * gr + 2);
+      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int u = 0; u < 8; ++u) kv[u] = kc[(int64_t)(4 * ((c0 + u + rot) & (D / 4 - 1))) * nB];
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[4 * ((c0 + u + rot) & (D / 4 - 1))], kv[u], acc, 0, 0, 0);
+      for (int g = 0; g < NG; ++g) {
+        const int gr = (g + rot) & (NG - 1);
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 0], kv[g][0].x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 1], kv[g][0].y, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 2], kv[g][1].x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 3], kv[g][1].y, acc, 0, 0, 0);
       }
       const int j = j0 + li;
       if (j < nB) {
@@ -374,65 +394,69 @@ __global__ void fill_ones_kernel(uint8_t *p, size_t n) {
 }  // namespace
 
 hipError_t launch_pool(View q, View k, int B, int H, int N, int d, int bs, double *qbar,
-                       double *kbarT, hipStream_t s) {
+                       double *kbar, hipStream_t s) {
   const int nB = (N + bs - 1) / bs;
   dim3 grid(nB, B * H, 2);
   if (d == 128)
-    hipLaunchKernelGGL(pool_kernel<128>, grid, dim3(256), 0, s, q, k, H, N, bs, nB, qbar, kbarT);
+    hipLaunchKernelGGL(pool_kernel<128>, grid, dim3(256), 0, s, q, k, H, N, bs, nB, qbar, kbar);
   else
-    hipLaunchKernelGGL(pool_kernel<64>, grid, dim3(256), 0, s, q, k, H, N, bs, nB, qbar, kbarT);
+    hipLaunchKernelGGL(pool_kernel<64>, grid, dim3(256), 0, s, q, k, H, N, bs, nB, qbar, kbar);
   return hipGetLastError();
 }
 
 template <int D, int R>
-static hipError_t launch_select_dr(const double *qbar, const double *kbarT, int BH, int nB,
+static hipError_t launch_select_dr(const double *qbar, const double *kbar, int BH, int nB,
                                    double sigma, double tau, uint8_t *mask, hipStream_t s) {
   const int G = (nB + R - 1) / R * BH;
   dim3 grid((G + 7) / 8 * 8);
-  const size_t lds = (size_t)R * (nB + D) * sizeof(double);
-  const int P = nB <= 64 ? 64 : (1 << (32 - __builtin_clz((unsigned)(nB - 1))));
+  const size_t lds = (size_t)R * (nB + D + 2) * sizeof(double);
+  const int need = (nB + 63) / 64;  // positions per lane
 #define CARNATOR_SEL(EE)                                                                          \
   do {                                                                                            \
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&select_kernel<D, EE, R>),  \
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);     \
     if (e != hipSuccess) return e;                                                                \
-    hipLaunchKernelGGL((select_kernel<D, EE, R>), grid, dim3(64 * R), lds, s, qbar, kbarT, nB,    \
+    hipLaunchKernelGGL((select_kernel<D, EE, R>), grid, dim3(64 * R), lds, s, qbar, kbar, nB,    \
                        sigma, tau, mask, BH);                                                     \
   } while (0)
-  switch (P / 64) {
-    case 1: CARNATOR_SEL(1); break;
-    case 2: CARNATOR_SEL(2); break;
-    case 4: CARNATOR_SEL(4); break;
-    case 8: CARNATOR_SEL(8); break;
-    case 16:
-      if constexpr (R <= 8) CARNATOR_SEL(16);
-      else return hipErrorInvalidValue;
-      break;
-    case 32:
-      if constexpr (R <= 8) CARNATOR_SEL(32);
-      else return hipErrorInvalidValue;
-      break;
-    default: return hipErrorInvalidValue;
+  // R = 16 (1024 threads, at most 128 VGPRs) only while a lane holds at most
+  // 8 positions; the launcher picks R accordingly
+  if (need <= 1) CARNATOR_SEL(1);
+  else if (need <= 2) CARNATOR_SEL(2);
+  else if (need <= 3) CARNATOR_SEL(3);
+  else if (need <= 4) CARNATOR_SEL(4);
+  else if (need <= 6) CARNATOR_SEL(6);
+  else if (need <= 8) CARNATOR_SEL(8);
+  else if constexpr (R <= 8) {
+    if (need <= 10) CARNATOR_SEL(10);
+    else if (need <= 12) CARNATOR_SEL(12);
+    else if (need <= 16) CARNATOR_SEL(16);
+    else if (need <= 24) CARNATOR_SEL(24);
+    else if (need <= 32) CARNATOR_SEL(32);
+    else return hipErrorInvalidValue;
+  } else {
+    return hipErrorInvalidValue;
   }
 #undef CARNATOR_SEL
   return hipGetLastError();
 }
 
 // R query blocks per workgroup (one wave each): their logits and pooled rows
-// take 8 R (nB + d) bytes of LDS, within 160 KiB for R = 8 up to nB = 2048.
+// take 8 R (nB + d + 2) bytes of LDS, within 160 KiB for R = 8 up to
+// nB = 2048.
 // R = 16 halves the kbar^T re-reads; it is used while a lane's share of a
 // row (E <= 8 positions) leaves the registers for 16 waves per workgroup.
 template <int D>
-static hipError_t launch_select_d(const double *qbar, const double *kbarT, int BH, int nB,
+static hipError_t launch_select_d(const double *qbar, const double *kbar, int BH, int nB,
                                   double sigma, double tau, uint8_t *mask, hipStream_t s) {
-  if (nB <= 512) return launch_select_dr<D, 16>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
-  return launch_select_dr<D, 8>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
+  if (nB <= 512) return launch_select_dr<D, 16>(qbar, kbar, BH, nB, sigma, tau, mask, s);
+  return launch_select_dr<D, 8>(qbar, kbar, BH, nB, sigma, tau, mask, s);
 }
 
-hipError_t launch_select(const double *qbar, const double *kbarT, int BH, int nB, int d,
+hipError_t launch_select(const double *qbar, const double *kbar, int BH, int nB, int d,
                          double sigma, double tau, uint8_t *mask, hipStream_t s) {
-  if (d == 128) return launch_select_d<128>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
-  return launch_select_d<64>(qbar, kbarT, BH, nB, sigma, tau, mask, s);
+  if (d == 128) return launch_select_d<128>(qbar, kbar, BH, nB, sigma, tau, mask, s);
+  return launch_select_d<64>(qbar, kbar, BH, nB, sigma, tau, mask, s);
 }
 
 hipError_t launch_fill_ones(uint8_t *p, size_t n, hipStream_t s) {
