@@ -95,10 +95,17 @@ __device__ int block_excl_scan(int v, int *sh, int *total) {
   return before;
 }
 
+// Rows up to which the lengths and both intermediate permutations of the
+// sort live in LDS (3 x 32 KiB beside the 32 KiB histogram) instead of HBM:
+// the passes are chains of dependent accesses, and in LDS each costs a few
+// hundred cycles instead of an L2 round trip.
+constexpr int64_t kLdsRows = 8192;
+
 // Single workgroup: row_ptr = exclusive scan of len, and a stable LSD radix
 // sort of the rows by key (nB - len), i.e. descending length, ascending row.
 // Each thread owns a contiguous range of rows, so every pass is stable.
-__global__ void __launch_bounds__(kScanThreads) scan_sort_kernel(const int32_t *__restrict__ len,
+template <bool IN_LDS>
+__global__ void __launch_bounds__(kScanThreads) scan_sort_kernel(const int32_t *__restrict__ len_g,
                                                                  int64_t R, int nB,
                                                                  int32_t *__restrict__ row_ptr,
                                                                  int32_t *__restrict__ order,
@@ -106,7 +113,16 @@ __global__ void __launch_bounds__(kScanThreads) scan_sort_kernel(const int32_t *
                                                                  int32_t *__restrict__ tmp1) {
   __shared__ int sh[kScanThreads / 64];
   __shared__ int hist[kBins][kScanThreads];
+  extern __shared__ int rows_lds[];  // IN_LDS: len [R], then two permutations [R]
   const int t = threadIdx.x;
+  const int32_t *len = len_g;
+  if constexpr (IN_LDS) {
+    for (int64_t r = t; r < R; r += kScanThreads) rows_lds[r] = len_g[r];
+    tmp0 = rows_lds + R;
+    tmp1 = rows_lds + 2 * R;
+    len = rows_lds;
+    __syncthreads();
+  }
   const int64_t per = (R + kScanThreads - 1) / kScanThreads;
   const int64_t lo = min<int64_t>(R, per * t), hi = min<int64_t>(R, lo + per);
 
@@ -159,7 +175,7 @@ __global__ void __launch_bounds__(kScanThreads) scan_sort_kernel(const int32_t *
       const int dig = ((nB - len[r]) >> shift) & (kBins - 1);
       dst[hist[dig][t]++] = r;
     }
-    __threadfence_block();
+    if constexpr (!IN_LDS) __threadfence_block();
     __syncthreads();
     src = dst;
   }
@@ -189,8 +205,17 @@ hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_p
   int32_t *tmp1 = reinterpret_cast<int32_t *>(ws + 2 * part);
   const unsigned g = (unsigned)((R + 3) / 4);
   hipLaunchKernelGGL(count_kernel, dim3(g), dim3(256), 0, s, mask, R, nB, len);
-  hipLaunchKernelGGL(scan_sort_kernel, dim3(1), dim3(kScanThreads), 0, s, len, R, nB, row_ptr,
-                     order, tmp0, tmp1);
+  if (R <= kLdsRows) {
+    const size_t lds = (size_t)3 * R * sizeof(int32_t);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&scan_sort_kernel<true>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(scan_sort_kernel<true>, dim3(1), dim3(kScanThreads), lds, s, len, R, nB,
+                       row_ptr, order, tmp0, tmp1);
+  } else {
+    hipLaunchKernelGGL(scan_sort_kernel<false>, dim3(1), dim3(kScanThreads), 0, s, len, R, nB,
+                       row_ptr, order, tmp0, tmp1);
+  }
   hipLaunchKernelGGL(fill_kernel, dim3(g), dim3(256), 0, s, mask, R, nB, row_ptr, col_idx);
   return hipGetLastError();
 }

@@ -155,7 +155,8 @@ def test_merge_bit_exact(wid):
     np.testing.assert_array_equal(got, oracle.merge_target_rows(m, rows, cols))
 
 
-@pytest.mark.parametrize("nb,density", [(3, 0.5), (139, 0.3), (256, 0.2), (931, 0.1)])
+# R = 5 nb rows: up to 8192 rows the sort runs in LDS, beyond it in HBM
+@pytest.mark.parametrize("nb,density", [(3, 0.5), (139, 0.3), (256, 0.2), (931, 0.1), (2048, 0.05)])
 def test_compaction_bit_exact(nb, density):
     m = synth.random_mask(1, 5, nb, density, nb)
     m[0, 1, 0] = 0
