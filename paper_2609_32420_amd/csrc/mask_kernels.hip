@@ -99,69 +99,6 @@ __device__ inline double key_value(uint64_t k) {
   return __longlong_as_double((long long)b);
 }
 
-// Cross-lane partner values for wave-wide reductions without LDS round
-// trips: quad permutes (lane ^ 1, lane ^ 2), the half-row and row mirrors
-// (lane 7 - i and 15 - i within 8 and 16 lanes) and the 16- and 32-lane
-// swaps.  After the steps below 2^s every lane of a 2^s-lane group holds the
-// group's value, so the mirrors pair each group with its sibling, and every
-// lane ends with the same result (each step combines the same two operands
-// in every lane; + and max are commutative).
-template <int O>
-__device__ inline uint32_t partner32(uint32_t x, int lane) {
-  if constexpr (O == 1) return __builtin_amdgcn_update_dpp(0u, x, 0xB1, 0xF, 0xF, false);
-  else if constexpr (O == 2) return __builtin_amdgcn_update_dpp(0u, x, 0x4E, 0xF, 0xF, false);
-  else if constexpr (O == 4) return __builtin_amdgcn_update_dpp(0u, x, 0x141, 0xF, 0xF, false);
-  else if constexpr (O == 8) return __builtin_amdgcn_update_dpp(0u, x, 0x140, 0xF, 0xF, false);
-  else if constexpr (O == 16) {
-    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
-    return (lane & 16) ? r[0] : r[1];
-  } else {
-    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-    return (lane & 32) ? r[0] : r[1];
-  }
-}
-template <int O>
-__device__ inline uint64_t partner64(uint64_t x, int lane) {
-  const uint32_t lo = partner32<O>((uint32_t)x, lane);
-  const uint32_t hi = partner32<O>((uint32_t)(x >> 32), lane);
-  return ((uint64_t)hi << 32) | lo;
-}
-template <int O>
-__device__ inline double partner_f64(double x, int lane) {
-  return __longlong_as_double((long long)partner64<O>((uint64_t)__double_as_longlong(x), lane));
-}
-template <typename T, typename F>
-__device__ inline T wave_reduce(T x, int lane, F op) {
-  if constexpr (sizeof(T) == 8 && !__is_same(T, double)) {
-    x = op(x, partner64<1>(x, lane));
-    x = op(x, partner64<2>(x, lane));
-    x = op(x, partner64<4>(x, lane));
-    x = op(x, partner64<8>(x, lane));
-    x = op(x, partner64<16>(x, lane));
-    x = op(x, partner64<32>(x, lane));
-  } else {
-    x = op(x, partner_f64<1>(x, lane));
-    x = op(x, partner_f64<2>(x, lane));
-    x = op(x, partner_f64<4>(x, lane));
-    x = op(x, partner_f64<8>(x, lane));
-    x = op(x, partner_f64<16>(x, lane));
-    x = op(x, partner_f64<32>(x, lane));
-  }
-  return x;
-}
-__device__ inline double wave_sum(double x, int lane) {
-  return wave_reduce(x, lane, [](double a, double b) { return a + b; });
-}
-__device__ inline double wave_max(double x, int lane) {
-  return wave_reduce(x, lane, [](double a, double b) { return fmax(a, b); });
-}
-__device__ inline uint64_t wave_min_u64(uint64_t x, int lane) {
-  return wave_reduce(x, lane, [](uint64_t a, uint64_t b) { return b < a ? b : a; });
-}
-__device__ inline uint64_t wave_max_u64(uint64_t x, int lane) {
-  return wave_reduce(x, lane, [](uint64_t a, uint64_t b) { return b > a ? b : a; });
-}
-
 // One workgroup of R waves per (bh, R consecutive query blocks).
 //
 // Phase 1, s_ij = sigma <qbar_i, kbar_j>: the R pooled query rows sit in LDS;
@@ -281,9 +218,9 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
         kmax = key[u] > kmax ? key[u] : kmax;
       }
     }
-    smax = wave_max(smax, lane);
-    kmin = wave_min_u64(kmin, lane);
-    kmax = wave_max_u64(kmax, lane);
+    smax = dpp_max(smax, lane);
+    kmin = dpp_min_u64(kmin, lane);
+    kmax = dpp_max_u64(kmax, lane);
     // softmax p = exp(s - max) / sum
     double lsum = 0.0;
 #pragma unroll
@@ -291,7 +228,7 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
       pl[u] = (u * 64 + lane < nB) ? exp(pl[u] - smax) : 0.0;
       lsum += pl[u];
     }
-    const double Z = wave_sum(lsum, lane);
+    const double Z = dpp_sum(lsum, lane);
 #pragma unroll
     for (int u = 0; u < E; ++u) pl[u] = pl[u] / Z;
 
@@ -306,7 +243,7 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
         c += __popcll(__ballot(ge));
       }
       cnt = c;
-      return wave_sum(m, lane);
+      return dpp_sum(m, lane);
     };
     int cnt_lo, cnt_hi = 0;
     uint64_t lo = kmin, hi = kmax + 1;
@@ -334,8 +271,8 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
             a = in && key[u] < a ? key[u] : a;
             b = in && key[u] > b ? key[u] : b;
           }
-          a = wave_min_u64(a, lane);
-          b = wave_max_u64(b, lane);
+          a = dpp_min_u64(a, lane);
+          b = dpp_max_u64(b, lane);
           // a < b: the interval holds at least two (distinct) keys
           K = b & ~((1ull << (63 - __clzll((long long)(a ^ b)))) - 1ull);
         }
@@ -356,7 +293,7 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
 #pragma unroll
       for (int u = 0; u < E; ++u)
         if (key[u] >= lo && key[u] < hi && key[u] > kl) kl = key[u];
-      kstar = wave_max_u64(kl, lane);
+      kstar = dpp_max_u64(kl, lane);
     }
     int k = 0;
 #pragma unroll
