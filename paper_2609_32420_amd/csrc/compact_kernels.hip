@@ -115,12 +115,24 @@ __global__ void __launch_bounds__(kScanThreads) scan_sort_kernel(const int32_t *
   __shared__ int hist[kBins][kScanThreads];
   extern __shared__ int rows_lds[];  // IN_LDS: len [R], then two permutations [R]
   const int t = threadIdx.x;
-  const int32_t *len = len_g;
+  // Accessors: with IN_LDS the arrays are indexed through the LDS array itself
+  // (plain LDS instructions; through a generic pointer every access would be a
+  // flat one, waiting on both the LDS and the memory counters).
+  auto lenv = [&](int64_t r) __attribute__((always_inline)) -> int {
+    if constexpr (IN_LDS) return rows_lds[r];
+    else return len_g[r];
+  };
+  auto perm_get = [&](int buf, int64_t x) __attribute__((always_inline)) -> int {
+    if constexpr (IN_LDS) return rows_lds[R * (1 + buf) + x];
+    else return (buf ? tmp1 : tmp0)[x];
+  };
+  auto perm_put = [&](bool last, int buf, int64_t pos, int r) __attribute__((always_inline)) {
+    if (last) order[pos] = r;
+    else if constexpr (IN_LDS) rows_lds[R * (1 + buf) + pos] = r;
+    else (buf ? tmp1 : tmp0)[pos] = r;
+  };
   if constexpr (IN_LDS) {
     for (int64_t r = t; r < R; r += kScanThreads) rows_lds[r] = len_g[r];
-    tmp0 = rows_lds + R;
-    tmp1 = rows_lds + 2 * R;
-    len = rows_lds;
     __syncthreads();
   }
   const int64_t per = (R + kScanThreads - 1) / kScanThreads;
@@ -128,27 +140,28 @@ __global__ void __launch_bounds__(kScanThreads) scan_sort_kernel(const int32_t *
 
   // ---- row_ptr
   int local = 0;
-  for (int64_t r = lo; r < hi; ++r) local += len[r];
+  for (int64_t r = lo; r < hi; ++r) local += lenv(r);
   int total;
   int run = block_excl_scan(local, sh, &total);
   for (int64_t r = lo; r < hi; ++r) {
     row_ptr[r] = run;
-    run += len[r];
+    run += lenv(r);
   }
   if (t == 0) row_ptr[R] = total;
 
-  // ---- order: key = nB - len, passes of 3 bits
+  // ---- order: key = nB - len, passes of 3 bits; pass p reads the
+  // permutation of pass p - 1 (buffer (p - 1) & 1; identity for p = 0) and
+  // writes buffer p & 1, the last pass `order`
   int passes = 0;
   for (int v = nB; v > 0; v >>= kRadixBits) ++passes;
-  const int32_t *src = nullptr;  // nullptr: identity permutation
   for (int p = 0; p < passes; ++p) {
     const int shift = p * kRadixBits;
-    int32_t *dst = (p == passes - 1) ? order : ((p & 1) ? tmp1 : tmp0);
+    const bool last = p == passes - 1;
 #pragma unroll
     for (int bin = 0; bin < kBins; ++bin) hist[bin][t] = 0;
     for (int64_t x = lo; x < hi; ++x) {
-      const int r = src ? src[x] : (int)x;
-      const int dig = ((nB - len[r]) >> shift) & (kBins - 1);
+      const int r = p ? perm_get((p - 1) & 1, x) : (int)x;
+      const int dig = ((nB - lenv(r)) >> shift) & (kBins - 1);
       hist[dig][t] += 1;
     }
     __syncthreads();
@@ -171,13 +184,12 @@ __global__ void __launch_bounds__(kScanThreads) scan_sort_kernel(const int32_t *
     }
     __syncthreads();
     for (int64_t x = lo; x < hi; ++x) {
-      const int r = src ? src[x] : (int)x;
-      const int dig = ((nB - len[r]) >> shift) & (kBins - 1);
-      dst[hist[dig][t]++] = r;
+      const int r = p ? perm_get((p - 1) & 1, x) : (int)x;
+      const int dig = ((nB - lenv(r)) >> shift) & (kBins - 1);
+      perm_put(last, p & 1, hist[dig][t]++, r);
     }
     if constexpr (!IN_LDS) __threadfence_block();
     __syncthreads();
-    src = dst;
   }
   if (passes == 0) {
     for (int64_t x = lo; x < hi; ++x) order[x] = (int)x;
