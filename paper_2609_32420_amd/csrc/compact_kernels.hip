@@ -132,7 +132,20 @@ __global__ void __launch_bounds__(kScanThreads) scan_sort_kernel(const int32_t *
     else (buf ? tmp1 : tmp0)[pos] = r;
   };
   if constexpr (IN_LDS) {
-    for (int64_t r = t; r < R; r += kScanThreads) rows_lds[r] = len_g[r];
+    // all of a thread's loads in flight at once (R <= kLdsRows), clamped
+    // indices instead of branches
+    constexpr int kPer = (int)(kLdsRows / kScanThreads);
+    int v[kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int64_t r = t + (int64_t)i * kScanThreads;
+      v[i] = len_g[r < R ? r : R - 1];
+    }
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int64_t r = t + (int64_t)i * kScanThreads;
+      if (r < R) rows_lds[r] = v[i];
+    }
     __syncthreads();
   }
   const int64_t per = (R + kScanThreads - 1) / kScanThreads;
