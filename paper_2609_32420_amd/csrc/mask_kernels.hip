@@ -99,7 +99,8 @@ __device__ inline double key_value(uint64_t k) {
   return __longlong_as_double((long long)b);
 }
 
-// One workgroup of R waves per (bh, R consecutive query blocks).
+// One workgroup of W waves per (bh, R consecutive query blocks), W = R or
+// R / 2 (then each wave selects two rows).
 //
 // Phase 1, s_ij = sigma <qbar_i, kbar_j>: the R pooled query rows sit in LDS;
 // a wave takes 16 key blocks at a time and forms the 16 x 16 tile of dot
@@ -111,8 +112,8 @@ __device__ inline double key_value(uint64_t k) {
 // its channels in the same order.  With R = 8 the upper half of the tile
 // repeats row R - 1 and is not stored.  Phase 2 gives each wave one row
 // (E = positions per lane, 64 E >= nB).
-template <int D, int E, int R>
-__global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict__ qbar,
+template <int D, int E, int R, int W>
+__global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict__ qbar,
                                                         const double *__restrict__ kbar, int nB,
                                                         double sigma, double tau,
                                                         uint8_t *__restrict__ mask, int BH) {
@@ -139,16 +140,16 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
 
   double *qs = sc + R * nB;
   {
-    constexpr int SPT = D / 64;  // staged values per thread (both loads in flight)
+    constexpr int SPT = R * D / (64 * W);  // staged values per thread (all loads in flight)
     double sv[SPT];
 #pragma unroll
     for (int i = 0; i < SPT; ++i) {
-      const int x = threadIdx.x + i * 64 * R, r = x / D, c = x - r * D;
+      const int x = threadIdx.x + i * 64 * W, r = x / D, c = x - r * D;
       sv[i] = qb[min(r, nr - 1) * D + c];
     }
 #pragma unroll
     for (int i = 0; i < SPT; ++i) {
-      const int x = threadIdx.x + i * 64 * R, r = x / D, c = x - r * D;
+      const int x = threadIdx.x + i * 64 * W, r = x / D, c = x - r * D;
       qs[r * QS + c] = sv[i];
     }
   }
@@ -161,7 +162,7 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
     // The groups start at a different place in every wave: walking them in
     // lockstep sends every wave of the chip to the same few L2 channels.
     const int rot = (wave * 5 + T * 3) & (NG - 1);
-    for (int j0 = wave * 16; j0 < nB; j0 += 16 * R) {
+    for (int j0 = wave * 16; j0 < nB; j0 += 16 * W) {
       const double *kr = kb + (int64_t)min(j0 + li, nB - 1) * D + 4 * lk;
       f64x4 acc = {0.0, 0.0, 0.0, 0.0};
       // All of the tile's loads are issued before the first product: left to
@@ -199,7 +200,7 @@ __global__ void __launch_bounds__(64 * R) select_kernel(const double *__restrict
   // u 64 + l.  The k-th largest sort key K* (k the shortest prefix whose
   // mass reaches tau) is found by bisection over the keys, keeping
   // mass(key >= lo) >= tau > mass(key >= hi) until [lo, hi) holds one key.
-  for (int r = wave; r < nr; r += R) {
+  for (int r = wave; r < nr; r += W) {
     const double *row = sc + r * nB;
     uint8_t *out = mask + ((int64_t)bh * nB + r0 + r) * nB;
     double pl[E];
@@ -341,7 +342,7 @@ hipError_t launch_pool(View q, View k, int B, int H, int N, int d, int bs, doubl
   return hipGetLastError();
 }
 
-template <int D, int R>
+template <int D, int R, int W>
 static hipError_t launch_select_dr(const double *qbar, const double *kbar, int BH, int nB,
                                    double sigma, double tau, uint8_t *mask, hipStream_t s) {
   const int G = (nB + R - 1) / R * BH;
@@ -350,27 +351,31 @@ static hipError_t launch_select_dr(const double *qbar, const double *kbar, int B
   const int need = (nB + 63) / 64;  // positions per lane
 #define CARNATOR_SEL(EE)                                                                          \
   do {                                                                                            \
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&select_kernel<D, EE, R>),  \
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&select_kernel<D, EE, R, W>), \
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);     \
     if (e != hipSuccess) return e;                                                                \
-    hipLaunchKernelGGL((select_kernel<D, EE, R>), grid, dim3(64 * R), lds, s, qbar, kbar, nB,    \
+    hipLaunchKernelGGL((select_kernel<D, EE, R, W>), grid, dim3(64 * W), lds, s, qbar, kbar, nB, \
                        sigma, tau, mask, BH);                                                     \
   } while (0)
-  // R = 16 (1024 threads, at most 128 VGPRs) only while a lane holds at most
-  // 8 positions; the launcher picks R accordingly
+  // W = 16 waves (1024 threads, at most 128 VGPRs) only while a lane holds at
+  // most 8 positions; the launcher picks R and W accordingly
   if (need <= 1) CARNATOR_SEL(1);
   else if (need <= 2) CARNATOR_SEL(2);
   else if (need <= 3) CARNATOR_SEL(3);
   else if (need <= 4) CARNATOR_SEL(4);
   else if (need <= 6) CARNATOR_SEL(6);
   else if (need <= 8) CARNATOR_SEL(8);
-  else if constexpr (R <= 8) {
+  else if constexpr (W <= 8) {
     if (need <= 10) CARNATOR_SEL(10);
     else if (need <= 12) CARNATOR_SEL(12);
     else if (need <= 16) CARNATOR_SEL(16);
-    else if (need <= 24) CARNATOR_SEL(24);
-    else if (need <= 32) CARNATOR_SEL(32);
-    else return hipErrorInvalidValue;
+    else if constexpr (R <= 8) {  // R = 16 serves nB <= 1024 only
+      if (need <= 24) CARNATOR_SEL(24);
+      else if (need <= 32) CARNATOR_SEL(32);
+      else return hipErrorInvalidValue;
+    } else {
+      return hipErrorInvalidValue;
+    }
   } else {
     return hipErrorInvalidValue;
   }
@@ -378,16 +383,18 @@ static hipError_t launch_select_dr(const double *qbar, const double *kbar, int B
   return hipGetLastError();
 }
 
-// R query blocks per workgroup (one wave each): their logits and pooled rows
-// take 8 R (nB + d + 2) bytes of LDS, within 160 KiB for R = 8 up to
-// nB = 2048.
-// R = 16 halves the kbar^T re-reads; it is used while a lane's share of a
-// row (E <= 8 positions) leaves the registers for 16 waves per workgroup.
+// R query blocks per workgroup: their logits and pooled rows take
+// 8 R (nB + d + 2) bytes of LDS, within 160 KiB for R = 16 up to nB = 1024
+// and for R = 8 up to nB = 2048.  R = 16 fills the 16-row fp64 MFMA tiles
+// and halves the kbar re-reads.  W = 16 waves (one row each) while a lane's
+// share of a row (E <= 8 positions) fits the 128 registers of a 1024-thread
+// workgroup, else W = 8 (two rows each when R = 16).
 template <int D>
 static hipError_t launch_select_d(const double *qbar, const double *kbar, int BH, int nB,
                                   double sigma, double tau, uint8_t *mask, hipStream_t s) {
-  if (nB <= 512) return launch_select_dr<D, 16>(qbar, kbar, BH, nB, sigma, tau, mask, s);
-  return launch_select_dr<D, 8>(qbar, kbar, BH, nB, sigma, tau, mask, s);
+  if (nB <= 512) return launch_select_dr<D, 16, 16>(qbar, kbar, BH, nB, sigma, tau, mask, s);
+  if (nB <= 1024) return launch_select_dr<D, 16, 8>(qbar, kbar, BH, nB, sigma, tau, mask, s);
+  return launch_select_dr<D, 8, 8>(qbar, kbar, BH, nB, sigma, tau, mask, s);
 }
 
 hipError_t launch_select(const double *qbar, const double *kbar, int BH, int nB, int d,
