@@ -79,20 +79,20 @@ __global__ void __launch_bounds__(256) pool_kernel(View q, View k, int H, int N,
 
 // ---- selection --------------------------------------------------------------
 //
-// Sort keys: an order-preserving map of the fp64 logit onto uint64 whose low
-// 11 bits are replaced by (2047 - block index).  Sorting the keys in
-// descending order is sorting by logit with the lower index first among
-// logits equal in their top 53 bits; logits closer than that (2^-42
-// relative) lie deep inside the 1e-6 tie band, where the final choice is made
-// by block index anyway.  The exact logit of each sorted entry is read back
-// by its index.
+// Selection keys: an order-preserving map of the fp64 logit onto uint64 whose
+// low 11 bits are replaced by (2047 - block index).  Descending key order is
+// descending logit with the lower index first among logits equal in their
+// top 53 bits; logits closer than that (2^-42 relative) lie deep inside the
+// 1e-6 tie band, where the final choice is made by block index anyway.  The
+// keys are unique; the selection finds the k-th largest by bisection and
+// reads back the exact logit of its block.
 __device__ inline uint64_t sel_key(double s, int j) {
   const uint64_t b = (uint64_t)__double_as_longlong(s);
   const uint64_t m = (b >> 63) ? ~b : (b | 0x8000000000000000ull);
   return (m & ~0x7ffull) | (uint64_t)(2047 - j);
 }
 __device__ inline int sel_index(uint64_t k) { return 2047 - (int)(k & 0x7ff); }
-// The logit a sort key stands for, up to its low 11 bits (used only to pick
+// The logit a selection key stands for, up to its low 11 bits (used only to pick
 // bisection points).
 __device__ inline double key_value(uint64_t k) {
   const uint64_t b = (k >> 63) ? (k & 0x7fffffffffffffffull) : ~k;
@@ -110,8 +110,8 @@ __device__ inline double key_value(uint64_t k) {
 // 16 g + 4 k .. 16 g + 4 k + 3 of key block i (one 32-byte piece of its kbar
 // row) and feeds channel 16 g + 4 k + t to step t, and the query side takes
 // its channels in the same order.  With R = 8 the upper half of the tile
-// repeats row R - 1 and is not stored.  Phase 2 gives each wave one row
-// (E = positions per lane, 64 E >= nB).
+// repeats row R - 1 and is not stored.  Phase 2: wave w selects rows w,
+// w + W, ... of the workgroup (E = positions per lane, 64 E >= nB).
 template <int D, int E, int R, int W>
 __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict__ qbar,
                                                         const double *__restrict__ kbar, int nB,
@@ -197,7 +197,7 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
   __syncthreads();
 
   // ---- phase 2: selection, one row per wave.  Lane l holds positions
-  // u 64 + l.  The k-th largest sort key K* (k the shortest prefix whose
+  // u 64 + l.  The k-th largest selection key K* (k the shortest prefix whose
   // mass reaches tau) is found by bisection over the keys, keeping
   // mass(key >= lo) >= tau > mass(key >= hi) until [lo, hi) holds one key.
   for (int r = wave; r < nr; r += W) {
