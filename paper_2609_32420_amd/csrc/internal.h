@@ -18,69 +18,67 @@ struct View {
 };
 
 // ---- wave-wide reductions (device code of every kernel file) ----------------
-// Cross-lane partner values for wave-wide reductions without LDS round
-// trips: quad permutes (lane ^ 1, lane ^ 2), the half-row and row mirrors
-// (lane 7 - i and 15 - i within 8 and 16 lanes) and the 16- and 32-lane
-// swaps.  After the steps below 2^s every lane of a 2^s-lane group holds the
-// group's value, so the mirrors pair each group with its sibling, and every
-// lane ends with the same result (each step combines the same two operands
-// in every lane; + and max are commutative).
-template <int O>
-__device__ inline uint32_t partner32(uint32_t x, int lane) {
-  if constexpr (O == 1) return __builtin_amdgcn_update_dpp(0u, x, 0xB1, 0xF, 0xF, false);
-  else if constexpr (O == 2) return __builtin_amdgcn_update_dpp(0u, x, 0x4E, 0xF, 0xF, false);
-  else if constexpr (O == 4) return __builtin_amdgcn_update_dpp(0u, x, 0x141, 0xF, 0xF, false);
-  else if constexpr (O == 8) return __builtin_amdgcn_update_dpp(0u, x, 0x140, 0xF, 0xF, false);
-  else if constexpr (O == 16) {
-    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
-    return (lane & 16) ? r[0] : r[1];
-  } else {
-    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-    return (lane & 32) ? r[0] : r[1];
-  }
-}
-template <int O>
-__device__ inline uint64_t partner64(uint64_t x, int lane) {
-  const uint32_t lo = partner32<O>((uint32_t)x, lane);
-  const uint32_t hi = partner32<O>((uint32_t)(x >> 32), lane);
+// x of lane l (l the same in every lane), in scalar registers.
+__device__ inline uint64_t read_lane(uint64_t x, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), l);
   return ((uint64_t)hi << 32) | lo;
 }
-template <int O>
-__device__ inline double partner_f64(double x, int lane) {
-  return __longlong_as_double((long long)partner64<O>((uint64_t)__double_as_longlong(x), lane));
+// A value that is the same in every lane, moved to scalar registers (the
+// compiler cannot prove it uniform by itself).
+__device__ inline bool uniform(bool x) { return __builtin_amdgcn_readfirstlane((int)x) != 0; }
+__device__ inline uint64_t uniform(uint64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
 }
-template <typename T, typename F>
-__device__ inline T dpp_reduce(T x, int lane, F op) {
-  if constexpr (sizeof(T) == 8 && !__is_same(T, double)) {
-    x = op(x, partner64<1>(x, lane));
-    x = op(x, partner64<2>(x, lane));
-    x = op(x, partner64<4>(x, lane));
-    x = op(x, partner64<8>(x, lane));
-    x = op(x, partner64<16>(x, lane));
-    x = op(x, partner64<32>(x, lane));
-  } else {
-    x = op(x, partner_f64<1>(x, lane));
-    x = op(x, partner_f64<2>(x, lane));
-    x = op(x, partner_f64<4>(x, lane));
-    x = op(x, partner_f64<8>(x, lane));
-    x = op(x, partner_f64<16>(x, lane));
-    x = op(x, partner_f64<32>(x, lane));
-  }
-  return x;
-}
-__device__ inline double dpp_sum(double x, int lane) {
-  return dpp_reduce(x, lane, [](double a, double b) { return a + b; });
-}
-__device__ inline double dpp_max(double x, int lane) {
-  return dpp_reduce(x, lane, [](double a, double b) { return fmax(a, b); });
-}
-__device__ inline uint64_t dpp_min_u64(uint64_t x, int lane) {
-  return dpp_reduce(x, lane, [](uint64_t a, uint64_t b) { return b < a ? b : a; });
-}
-__device__ inline uint64_t dpp_max_u64(uint64_t x, int lane) {
-  return dpp_reduce(x, lane, [](uint64_t a, uint64_t b) { return b > a ? b : a; });
+__device__ inline double uniform(double x) {
+  return __longlong_as_double((long long)uniform((uint64_t)__double_as_longlong(x)));
 }
 
+// 64-bit DPP move: CTRL is the DPP control, ROWS the 16-lane rows written
+// (the others are left undefined).
+template <int CTRL, int ROWS>
+__device__ inline uint64_t dpp64(uint64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)x, CTRL, ROWS, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)(x >> 32), CTRL, ROWS, 0xF, false);
+  return ((uint64_t)hi << 32) | lo;
+}
+// Wave-wide reduction to a scalar.  Four DPP steps combine each lane with
+// lane ^ 1 and lane ^ 2 (quad permutes), then with its half-row and row
+// mirrors (7 - i within 8 lanes, 15 - i within 16), after which every lane of
+// a 16-lane row holds the row's value; two row broadcasts then add row 0
+// into row 1 and row 2 into row 3 (lanes 15 and 47), and row 1 into row 3
+// (lane 31), so that lane 63 holds the wave's value.  Lanes outside the rows
+// a broadcast writes end with values that are never read.  The order of
+// combination is fixed, so the result does not depend on scheduling.
+template <typename F>
+__device__ inline uint64_t wave_reduce_bits(uint64_t x, F op) {
+  x = op(x, dpp64<0xB1, 0xF>(x));   // quad_perm [1, 0, 3, 2]
+  x = op(x, dpp64<0x4E, 0xF>(x));   // quad_perm [2, 3, 0, 1]
+  x = op(x, dpp64<0x141, 0xF>(x));  // row_half_mirror
+  x = op(x, dpp64<0x140, 0xF>(x));  // row_mirror
+  x = op(x, dpp64<0x142, 0xA>(x));  // row_bcast:15 into rows 1 and 3
+  x = op(x, dpp64<0x143, 0xC>(x));  // row_bcast:31 into rows 2 and 3
+  return read_lane(x, 63);
+}
+__device__ inline double bits_f64(uint64_t x) { return __longlong_as_double((long long)x); }
+__device__ inline uint64_t f64_bits(double x) { return (uint64_t)__double_as_longlong(x); }
+__device__ inline double wave_sum(double x) {
+  return bits_f64(wave_reduce_bits(f64_bits(x), [](uint64_t a, uint64_t b) { return f64_bits(bits_f64(a) + bits_f64(b)); }));
+}
+__device__ inline double wave_max(double x) {
+  return bits_f64(wave_reduce_bits(f64_bits(x), [](uint64_t a, uint64_t b) { return f64_bits(fmax(bits_f64(a), bits_f64(b))); }));
+}
+__device__ inline double wave_min(double x) {
+  return bits_f64(wave_reduce_bits(f64_bits(x), [](uint64_t a, uint64_t b) { return f64_bits(fmin(bits_f64(a), bits_f64(b))); }));
+}
+__device__ inline uint64_t wave_min_u64(uint64_t x) {
+  return wave_reduce_bits(x, [](uint64_t a, uint64_t b) { return b < a ? b : a; });
+}
+__device__ inline uint64_t wave_max_u64(uint64_t x) {
+  return wave_reduce_bits(x, [](uint64_t a, uint64_t b) { return b > a ? b : a; });
+}
 
 // ---- block mask builder ----------------------------------------------------
 // Pools Q_hist and K_hist per block (fp64 means over valid tokens).

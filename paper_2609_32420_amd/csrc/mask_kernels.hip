@@ -200,28 +200,27 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
   // u 64 + l.  The k-th largest selection key K* (k the shortest prefix whose
   // mass reaches tau) is found by bisection over the keys, keeping
   // mass(key >= lo) >= tau > mass(key >= hi) until [lo, hi) holds one key.
+  // The bisection state is the same in every lane and lives in scalar
+  // registers; the vector work per step is one compare and add per position
+  // and one wave sum.
   for (int r = wave; r < nr; r += W) {
     const double *row = sc + r * nB;
     uint8_t *out = mask + ((int64_t)bh * nB + r0 + r) * nB;
     double pl[E];
     uint64_t key[E];
-    double smax = -INFINITY;
-    uint64_t kmin = ~0ull, kmax = 0ull;
+    double smax = -INFINITY, smin = INFINITY;
 #pragma unroll
     for (int u = 0; u < E; ++u) {
       const int p = u * 64 + lane;
       const bool ok = p < nB;
-      pl[u] = ok ? row[p] : -INFINITY;  // the logit until the softmax below
-      key[u] = ok ? sel_key(pl[u], p) : 0ull;  // valid keys are > 2047
+      const double s = row[min(p, nB - 1)];
+      pl[u] = ok ? s : -INFINITY;  // the logit until the softmax below
+      key[u] = ok ? sel_key(s, p) : 0ull;  // valid keys are > 2047
       smax = fmax(smax, pl[u]);
-      if (ok) {
-        kmin = key[u] < kmin ? key[u] : kmin;
-        kmax = key[u] > kmax ? key[u] : kmax;
-      }
+      smin = ok ? fmin(smin, s) : smin;
     }
-    smax = dpp_max(smax, lane);
-    kmin = dpp_min_u64(kmin, lane);
-    kmax = dpp_max_u64(kmax, lane);
+    smax = wave_max(smax);
+    smin = wave_min(smin);
     // softmax p = exp(s - max) / sum
     double lsum = 0.0;
 #pragma unroll
@@ -229,7 +228,7 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
       pl[u] = (u * 64 + lane < nB) ? exp(pl[u] - smax) : 0.0;
       lsum += pl[u];
     }
-    const double Z = dpp_sum(lsum, lane);
+    const double Z = wave_sum(lsum);
 #pragma unroll
     for (int u = 0; u < E; ++u) pl[u] = pl[u] / Z;
 
@@ -244,13 +243,16 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
         c += __popcll(__ballot(ge));
       }
       cnt = c;
-      return dpp_sum(m, lane);
+      return wave_sum(m) >= tau;
     };
+    // every key lies in [smallest key of value smin, largest key of smax]
+    uint64_t lo = sel_key(smin, 2047), hi = sel_key(smax, 0) + 1;
     int cnt_lo, cnt_hi = 0;
-    uint64_t lo = kmin, hi = kmax + 1;
-    uint64_t kstar;
-    if (!(mass_ge(lo, cnt_lo) >= tau)) {
-      kstar = kmin;  // the whole row falls short of tau: keep every block
+    int k;
+    double cut;
+    if (!mass_ge(lo, cnt_lo)) {
+      k = cnt_lo;  // the whole row falls short of tau: keep every block
+      cut = smin;
     } else {
       // Split at the midpoint of the values while that separates keys; once
       // it does not (a run of equal logits), split at the highest bit in
@@ -261,7 +263,7 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
         uint64_t K = 0;
         if (!trie) {
           const double lv = key_value(lo), hv = key_value(hi - 1);
-          K = sel_key(lv + 0.5 * (hv - lv), 2047);
+          K = sel_key(uniform(lv + 0.5 * (hv - lv)), 2047);
           trie = !(K > lo && K < hi);
         }
         if (trie) {
@@ -272,15 +274,14 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
             a = in && key[u] < a ? key[u] : a;
             b = in && key[u] > b ? key[u] : b;
           }
-          a = dpp_min_u64(a, lane);
-          b = dpp_max_u64(b, lane);
+          a = wave_min_u64(a);
+          b = wave_max_u64(b);
           // a < b: the interval holds at least two (distinct) keys
           K = b & ~((1ull << (63 - __clzll((long long)(a ^ b)))) - 1ull);
         }
         const int before = cnt_lo - cnt_hi;
         int c;
-        const bool up = __builtin_amdgcn_readfirstlane((int)(mass_ge(K, c) >= tau)) != 0;
-        if (up) {
+        if (mass_ge(K, c)) {
           lo = K;
           cnt_lo = c;
         } else {
@@ -289,17 +290,28 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
         }
         if (cnt_lo - cnt_hi == before) trie = true;
       }
-      // the largest key in [lo, hi) (the only one, unless the cap was hit)
-      uint64_t kl = 0ull;
+      uint64_t kstar = 0ull;
+      if (cnt_lo - cnt_hi == 1) {
+        // the one key in [lo, hi), read from the lane that holds it
 #pragma unroll
-      for (int u = 0; u < E; ++u)
-        if (key[u] >= lo && key[u] < hi && key[u] > kl) kl = key[u];
-      kstar = dpp_max_u64(kl, lane);
+        for (int u = 0; u < E; ++u) {
+          const unsigned long long bits = __ballot(key[u] >= lo && key[u] < hi);
+          if (bits) kstar = read_lane(key[u], __ffsll((long long)bits) - 1);
+        }
+        k = cnt_lo;
+      } else {
+        // the step cap was hit: the largest key in [lo, hi)
+        uint64_t kl = 0ull;
+#pragma unroll
+        for (int u = 0; u < E; ++u)
+          if (key[u] >= lo && key[u] < hi && key[u] > kl) kl = key[u];
+        kstar = wave_max_u64(kl);
+        k = 0;
+#pragma unroll
+        for (int u = 0; u < E; ++u) k += __popcll(__ballot(key[u] >= kstar));
+      }
+      cut = row[sel_index(kstar)];
     }
-    int k = 0;
-#pragma unroll
-    for (int u = 0; u < E; ++u) k += __popcll(__ballot(key[u] >= kstar));
-    const double cut = row[sel_index(kstar)];
     const double hiT = cut + kTieEps;
 
     // |S+| : blocks strictly above the tie band
