@@ -221,18 +221,17 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
     }
     smax = wave_max(smax);
     smin = wave_min(smin);
-    // softmax p = exp(s - max) / sum
+    // softmax weights exp(s - max): a set's mass p = weight / Z reaches tau
+    // when its weight reaches tau Z (Z the sum of all weights)
     double lsum = 0.0;
 #pragma unroll
     for (int u = 0; u < E; ++u) {
       pl[u] = (u * 64 + lane < nB) ? exp(pl[u] - smax) : 0.0;
       lsum += pl[u];
     }
-    const double Z = wave_sum(lsum);
-#pragma unroll
-    for (int u = 0; u < E; ++u) pl[u] = pl[u] / Z;
+    const double tauZ = tau * wave_sum(lsum);
 
-    // mass and count of the keys >= K (identical in every lane)
+    // whether the keys >= K reach tau, and their count (the same in every lane)
     auto mass_ge = [&](uint64_t K, int &cnt) __attribute__((always_inline)) {
       double m = 0.0;
       int c = 0;
@@ -243,7 +242,7 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
         c += __popcll(__ballot(ge));
       }
       cnt = c;
-      return wave_sum(m) >= tau;
+      return wave_sum(m) >= tauZ;
     };
     // every key lies in [smallest key of value smin, largest key of smax]
     uint64_t lo = sel_key(smin, 2047), hi = sel_key(smax, 0) + 1;
