@@ -216,12 +216,14 @@ __device__ inline void tk_rounds(const double (&vals)[kTkRegs], bool in_regs, co
 // Top-k with a candidate filter.  The rows are split into 64 groups (16
 // lanes of a wave, all their rows); the topk-th largest group maximum theta
 // is a lower bound of the topk-th largest value, since topk groups each hold
-// a row at or above it.  Rows with key >= theta are compacted into LDS and
-// ranked by one wave.  When there are more than 64 candidates, or topk > 16,
-// or the bank is too large for registers, the rounds above give the ordered
-// top-k instead.  The tie rule then needs the number of rows within eps of the
-// cut; when that equals the number of picks at or below cut + eps the picks
-// already are the answer, otherwise further rounds take the lowest tied rows.
+// a row at or above it.  Every row at or above theta - eps is a candidate:
+// that set holds the top k and every row within eps of the k-th value, so
+// when it has at most 64 rows one wave finishes the selection from it, tie
+// rule included.  With more candidates, or a bank too large for registers,
+// the rounds above give the ordered top k and the tie rule counts over all
+// rows: when the rows within eps of the cut are exactly the picks at or below
+// cut + eps the picks are the answer, otherwise further rounds take the
+// lowest tied rows.
 __global__ void __launch_bounds__(kTkThreads) topk_kernel(const double *__restrict__ sims, int64_t m,
                                                            int topk, int32_t *__restrict__ idx_out,
                                                            float *__restrict__ sim_out) {
@@ -229,6 +231,8 @@ __global__ void __launch_bounds__(kTkThreads) topk_kernel(const double *__restri
   const double *sv = sims + (int64_t)blockIdx.x * m;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const bool in_regs = m <= (int64_t)kTkThreads * kTkRegs;
+  int32_t *io = idx_out + (int64_t)blockIdx.x * topk;
+  float *so = sim_out + (int64_t)blockIdx.x * topk;
   double vals[kTkRegs];
   if (in_regs) {
 #pragma unroll
@@ -237,8 +241,7 @@ __global__ void __launch_bounds__(kTkThreads) topk_kernel(const double *__restri
       vals[u] = x < m ? sv[x] : 0.0;
     }
   }
-  bool ranked = false;
-  if (in_regs && topk <= 16) {
+  if (in_regs) {
     uint64_t g = 0;
 #pragma unroll
     for (int u = 0; u < kTkRegs; ++u) {
@@ -246,10 +249,17 @@ __global__ void __launch_bounds__(kTkThreads) topk_kernel(const double *__restri
       const uint64_t k = okey(vals[u]);
       g = (x < m && k > g) ? k : g;
     }
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) {
-      const uint64_t og = (uint64_t)__shfl_xor((long long)g, o);
-      g = og > g ? og : g;
+    // maximum over the 16 lanes of a row (lane ^ 1, lane ^ 2, half-row and
+    // row mirrors: every lane ends with the row's value)
+    {
+      uint64_t o = dpp64<0xB1, 0xF>(g);
+      g = o > g ? o : g;
+      o = dpp64<0x4E, 0xF>(g);
+      g = o > g ? o : g;
+      o = dpp64<0x141, 0xF>(g);
+      g = o > g ? o : g;
+      o = dpp64<0x140, 0xF>(g);
+      g = o > g ? o : g;
     }
     if ((lane & 15) == 0) sh.gmax[w * 4 + (lane >> 4)] = g;
     if (t == 0) sh.ncand = 0;
@@ -266,12 +276,13 @@ __global__ void __launch_bounds__(kTkThreads) topk_kernel(const double *__restri
       if (lane == __ffsll((long long)hit) - 1) sh.theta = mine;
     }
     __syncthreads();
-    const uint64_t theta = sh.theta;
+    // (theta = 0 when it comes from a group without rows: every row qualifies)
+    const uint64_t th = sh.theta;
+    const double low = th == 0 ? -INFINITY : okey_value(th) - kTieEps;
 #pragma unroll
     for (int u = 0; u < kTkRegs; ++u) {
       const int64_t x = t + (int64_t)kTkThreads * u;
-      const uint64_t k = okey(vals[u]);
-      const bool c = x < m && k >= theta;
+      const bool c = x < m && vals[u] >= low;
       const unsigned long long bits = __ballot(c);
       if (bits) {
         int base = 0;
@@ -279,7 +290,7 @@ __global__ void __launch_bounds__(kTkThreads) topk_kernel(const double *__restri
         base = __shfl(base, 0);
         const int pos = base + __popcll(bits & ((1ull << lane) - 1ull));
         if (c && pos < 64) {
-          sh.ck[pos] = k;
+          sh.ck[pos] = okey(vals[u]);
           sh.cx[pos] = (int)x;
         }
       }
@@ -287,24 +298,43 @@ __global__ void __launch_bounds__(kTkThreads) topk_kernel(const double *__restri
     __syncthreads();
     const int nc = sh.ncand;
     if (nc <= 64) {
-      if (w == 0) {
-        uint64_t k = 0;
-        int x = 0x7fffffff;
-        if (lane < nc) {
-          k = sh.ck[lane];
-          x = sh.cx[lane];
-        }
-        int rank = 0;
-        for (int j = 0; j < nc; ++j) rank += kbetter(sh.ck[j], sh.cx[j], k, x) ? 1 : 0;
-        if (lane < nc && rank < topk) {
-          sh.rk[rank] = k;
-          sh.rx[rank] = x;
-        }
+      if (w != 0) return;
+      // one wave: lane l < nc holds candidate l
+      const bool on = lane < nc;
+      uint64_t k = 0;
+      int x = 0x7fffffff;
+      if (on) {
+        k = sh.ck[lane];
+        x = sh.cx[lane];
       }
-      ranked = true;
+      int rank = 0;
+      for (int j = 0; j < nc; ++j) rank += kbetter(sh.ck[j], sh.cx[j], k, x) ? 1 : 0;
+      const double v = okey_value(k);
+      const unsigned long long at_cut = __ballot(on && rank == topk - 1);
+      const double cut = __shfl(v, __ffsll((long long)at_cut) - 1);
+      const bool above = on && v > cut + kTieEps;
+      const bool tie = on && fabs(v - cut) <= kTieEps;
+      const int need = topk - __popcll(__ballot(above));
+      // a tied row's place among the tied rows by row index
+      const unsigned long long tied = __ballot(tie);
+      int trank = 0;
+      for (unsigned long long b = tied; b; b &= b - 1ull) trank += sh.cx[__ffsll((long long)b) - 1] < x ? 1 : 0;
+      const bool pick = above || (tie && trank < need);
+      // output slot: picks in descending value, lower row first
+      const unsigned long long picks = __ballot(pick);
+      int slot = 0;
+      for (unsigned long long b = picks; b; b &= b - 1ull) {
+        const int j = __ffsll((long long)b) - 1;
+        slot += kbetter(sh.ck[j], sh.cx[j], k, x) ? 1 : 0;
+      }
+      if (pick) {
+        io[slot] = x;
+        so[slot] = (float)v;
+      }
+      return;
     }
   }
-  if (!ranked) tk_rounds<0>(vals, in_regs, sv, m, topk, 0.0, sh, 0);
+  tk_rounds<0>(vals, in_regs, sv, m, topk, 0.0, sh, 0);
   __syncthreads();
   const double cut = okey_value(sh.rk[topk - 1]);
   int nplus = 0;
@@ -328,8 +358,6 @@ __global__ void __launch_bounds__(kTkThreads) topk_kernel(const double *__restri
   int tied = 0;
 #pragma unroll
   for (int q = 0; q < kTkWaves; ++q) tied += sh.cnt[q];
-  int32_t *io = idx_out + (int64_t)blockIdx.x * topk;
-  float *so = sim_out + (int64_t)blockIdx.x * topk;
   if (tied == need) {
     if (t < topk) {
       io[t] = sh.rx[t];

@@ -364,6 +364,29 @@ def test_signature_shapes(m, dim, ld, nq, k):
     _check_topk(idx, sim, q.cpu().numpy(), bank.cpu().numpy(), k)
 
 
+@pytest.mark.parametrize("n_top,n_tied,k", [(3, 10, 8), (0, 30, 20), (3, 61, 50), (5, 2, 6), (1, 1, 2)])
+def test_signature_tie_band_among_few_candidates(n_top, n_tied, k):
+    # Unit vectors in a plane: n_top rows at cosine 1, n_tied rows a few 1e-9
+    # apart around cosine 0.999 (one tie band), every other row at cosine
+    # <= 0.71.  The cut falls inside the band, so the rule keeps its lowest
+    # rows; the candidates stay few, which is the single-wave selection.
+    m = 5000
+    rng = np.random.default_rng(1000 * n_top + n_tied)
+    theta = rng.uniform(np.pi / 4, 2 * np.pi - np.pi / 4, m)
+    rows = rng.choice(m, n_top + n_tied, replace=False)
+    theta[rows[:n_top]] = 0.0
+    theta[rows[n_top:]] = 0.0447 + 1e-7 * rng.random(n_tied)
+    bank = np.zeros((m, 4), np.float32)
+    bank[:, 0] = np.cos(theta)
+    bank[:, 1] = np.sin(theta)
+    q = np.array([[1.0, 0.0, 0.0, 0.0]], np.float32)
+    idx, sim = P.signature_sim(torch.as_tensor(q, device=DEV), torch.as_tensor(bank, device=DEV), k)
+    torch.cuda.synchronize()
+    _check_topk(idx, sim, q, bank, k)
+    wi, _, _ = oracle.topk_cosine(q, bank, k)
+    assert idx[0].tolist() == wi[0].tolist()
+
+
 @pytest.mark.parametrize("m", [10, 3000, 9000])
 def test_signature_ties_lower_row(m):
     # Row 7 is parallel to the query (cosine 1); the others sit 5e-11 below.
