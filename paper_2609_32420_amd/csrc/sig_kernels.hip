@@ -17,12 +17,6 @@ namespace {
 constexpr double kTieEps = 1e-6;
 constexpr int kQChunk = 4;  // queries scored per pass over the bank
 
-__device__ inline double wave_sum(double x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-  return x;
-}
-
 // One wave per bank row (grid-stride).  Scores queries [q0, q0 + nqc).  The
 // wave streams its bank row and the query rows kU float4 per lane at a time,
 // so the loads of a row are in flight together.  |q|^2 is accumulated in the
