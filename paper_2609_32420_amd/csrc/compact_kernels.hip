@@ -63,29 +63,31 @@ __global__ void __launch_bounds__(256) fill_kernel(const uint8_t *__restrict__ m
 }
 
 constexpr int kScanThreads = 1024;
-constexpr int kRadixBits = 3;
-constexpr int kBins = 1 << kRadixBits;
+
+// Inclusive scan over the 64 lanes of a wave: four DPP row shifts (by 1, 2,
+// 4, 8 lanes; lanes shifted in from outside the 16-lane row read 0) scan each
+// row, then two row broadcasts add lane 15 into row 1, lane 47 into row 3
+// and lane 31 into rows 2 and 3.
+__device__ inline int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31
+  return x;
+}
 
 // Block-wide exclusive scan of one int per thread (1024 threads); returns the
 // exclusive prefix and writes the total to *total.
 __device__ int block_excl_scan(int v, int *sh, int *total) {
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
+  const int x = wave_incl_scan(v);
   if (lane == 63) sh[w] = x;
   __syncthreads();
   if (w == 0) {
-    int s = lane < kScanThreads / 64 ? sh[lane] : 0;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(s, o);
-      if (lane >= o) s += y;
-    }
+    const int s = wave_incl_scan(lane < kScanThreads / 64 ? sh[lane] : 0);
     if (lane < kScanThreads / 64) sh[lane] = s;
   }
   __syncthreads();
@@ -95,117 +97,133 @@ __device__ int block_excl_scan(int v, int *sh, int *total) {
   return before;
 }
 
-// Rows up to which the lengths and both intermediate permutations of the
-// sort live in LDS (3 x 32 KiB beside the 32 KiB histogram) instead of HBM:
-// the passes are chains of dependent accesses, and in LDS each costs a few
-// hundred cycles instead of an L2 round trip.
-constexpr int64_t kLdsRows = 8192;
+// LDS budget of the counting sort: its counters and, when they fit beside
+// them, the row lengths.
+constexpr size_t kCountSortLds = 152 * 1024;
 
-// Single workgroup: row_ptr = exclusive scan of len, and a stable LSD radix
-// sort of the rows by key (nB - len), i.e. descending length, ascending row.
-// Each thread owns a contiguous range of rows, so every pass is stable.
-template <bool IN_LDS>
-__global__ void __launch_bounds__(kScanThreads) scan_sort_kernel(const int32_t *__restrict__ len_g,
-                                                                 int64_t R, int nB,
-                                                                 int32_t *__restrict__ row_ptr,
-                                                                 int32_t *__restrict__ order,
-                                                                 int32_t *__restrict__ tmp0,
-                                                                 int32_t *__restrict__ tmp1) {
-  __shared__ int sh[kScanThreads / 64];
-  __shared__ int hist[kBins][kScanThreads];
-  extern __shared__ int rows_lds[];  // IN_LDS: len [R], then two permutations [R]
-  const int t = threadIdx.x;
-  // Accessors: with IN_LDS the arrays are indexed through the LDS array itself
-  // (plain LDS instructions; through a generic pointer every access would be a
-  // flat one, waiting on both the LDS and the memory counters).
-  auto lenv = [&](int64_t r) __attribute__((always_inline)) -> int {
-    if constexpr (IN_LDS) return rows_lds[r];
+// Single workgroup: row_ptr = exclusive scan of the list lengths, and the
+// order of rows by descending length (lower row first on equal lengths) as a
+// counting sort on the length.  Wave w owns the contiguous rows
+// [w C, (w + 1) C) and walks them 64 at a time in row order.
+//   row_ptr: each wave sums its rows, the 16 wave totals give each wave its
+//     first offset, and a second walk writes the offsets with wave scans.
+//   order: pass 1 counts rows per (length, wave) with LDS atomics; an
+//     exclusive scan in (length descending, wave) order turns the counts into
+//     the first slot of each (length, wave) group; pass 2 walks the rows again
+//     in order: lanes holding equal lengths find each other with one ballot
+//     per key bit, each takes its group's next slot plus its rank among those
+//     lanes, and the lowest of them advances the counter.  Lengths descend,
+//     waves and rows ascend: the order the oracle defines.
+// LDS: uint32 counters [nB + 1][16] (index (nB - L) 16 + w), then with
+// LEN_LDS the lengths as uint16 [R]; otherwise they are read from len_g.
+template <bool LEN_LDS>
+__global__ void __launch_bounds__(kScanThreads) count_sort_kernel(const int32_t *__restrict__ len_g,
+                                                                  int R, int nB,
+                                                                  int32_t *__restrict__ row_ptr,
+                                                                  int32_t *__restrict__ order) {
+  constexpr int kWaves = kScanThreads / 64;
+  __shared__ int sh[kWaves];
+  extern __shared__ uint32_t cnt[];
+  const int K = (nB + 1) * kWaves;
+  uint16_t *len16 = reinterpret_cast<uint16_t *>(cnt + K);
+  const int t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  for (int i = t; i < K; i += kScanThreads) cnt[i] = 0;
+  if constexpr (LEN_LDS) {
+    // eight loads in flight per thread, clamped indices
+    for (int r0 = 0; r0 < R; r0 += 8 * kScanThreads) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int r = r0 + u * kScanThreads + t;
+        v[u] = len_g[r < R ? r : R - 1];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int r = r0 + u * kScanThreads + t;
+        if (r < R) len16[r] = (uint16_t)v[u];
+      }
+    }
+  }
+  __syncthreads();
+  auto lenv = [&](int r) __attribute__((always_inline)) -> int {
+    if constexpr (LEN_LDS) return len16[r];
     else return len_g[r];
   };
-  auto perm_get = [&](int buf, int64_t x) __attribute__((always_inline)) -> int {
-    if constexpr (IN_LDS) return rows_lds[R * (1 + buf) + x];
-    else return (buf ? tmp1 : tmp0)[x];
-  };
-  auto perm_put = [&](bool last, int buf, int64_t pos, int r) __attribute__((always_inline)) {
-    if (last) order[pos] = r;
-    else if constexpr (IN_LDS) rows_lds[R * (1 + buf) + pos] = r;
-    else (buf ? tmp1 : tmp0)[pos] = r;
-  };
-  if constexpr (IN_LDS) {
-    // all of a thread's loads in flight at once (R <= kLdsRows), clamped
-    // indices instead of branches
-    constexpr int kPer = (int)(kLdsRows / kScanThreads);
-    int v[kPer];
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int64_t r = t + (int64_t)i * kScanThreads;
-      v[i] = len_g[r < R ? r : R - 1];
-    }
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int64_t r = t + (int64_t)i * kScanThreads;
-      if (r < R) rows_lds[r] = v[i];
-    }
-    __syncthreads();
-  }
-  const int64_t per = (R + kScanThreads - 1) / kScanThreads;
-  const int64_t lo = min<int64_t>(R, per * t), hi = min<int64_t>(R, lo + per);
+  const int C = (R + kWaves - 1) / kWaves;
+  const int rlo = min(R, w * C), rhi = min(R, rlo + C);
 
   // ---- row_ptr
-  int local = 0;
-  for (int64_t r = lo; r < hi; ++r) local += lenv(r);
-  int total;
-  int run = block_excl_scan(local, sh, &total);
-  for (int64_t r = lo; r < hi; ++r) {
-    row_ptr[r] = run;
-    run += lenv(r);
+  {
+    int part = 0;
+    for (int r0 = rlo; r0 < rhi; r0 += 64) {
+      const int r = r0 + lane;
+      part += r < rhi ? lenv(r) : 0;
+    }
+    const int wtot = __builtin_amdgcn_readlane(wave_incl_scan(part), 63);
+    if (lane == 0) sh[w] = wtot;
+    __syncthreads();
+    int off = 0, total = 0;
+    for (int q = 0; q < kWaves; ++q) {
+      const int c = sh[q];
+      off += q < w ? c : 0;
+      total += c;
+    }
+    for (int r0 = rlo; r0 < rhi; r0 += 64) {
+      const int r = r0 + lane;
+      const int v = r < rhi ? lenv(r) : 0;
+      const int incl = wave_incl_scan(v);
+      if (r < rhi) row_ptr[r] = off + incl - v;
+      off += __builtin_amdgcn_readlane(incl, 63);
+    }
+    if (t == 0) row_ptr[R] = total;
   }
-  if (t == 0) row_ptr[R] = total;
 
-  // ---- order: key = nB - len, passes of 3 bits; pass p reads the
-  // permutation of pass p - 1 (buffer (p - 1) & 1; identity for p = 0) and
-  // writes buffer p & 1, the last pass `order`
-  int passes = 0;
-  for (int v = nB; v > 0; v >>= kRadixBits) ++passes;
-  for (int p = 0; p < passes; ++p) {
-    const int shift = p * kRadixBits;
-    const bool last = p == passes - 1;
-#pragma unroll
-    for (int bin = 0; bin < kBins; ++bin) hist[bin][t] = 0;
-    for (int64_t x = lo; x < hi; ++x) {
-      const int r = p ? perm_get((p - 1) & 1, x) : (int)x;
-      const int dig = ((nB - lenv(r)) >> shift) & (kBins - 1);
-      hist[dig][t] += 1;
+  // ---- order
+  int kbits = 0;
+  while ((1 << kbits) <= nB) ++kbits;
+  // the lanes of this walk step holding the same length as this lane
+  auto peers_of = [&](bool on, int L) __attribute__((always_inline)) {
+    unsigned long long m = __ballot(on);
+    for (int b = 0; b < kbits; ++b) {
+      const unsigned long long ones = __ballot(on && ((L >> b) & 1));
+      m &= ((L >> b) & 1) ? ones : ~ones;
     }
-    __syncthreads();
-    // exclusive scan over hist in (bin, thread) order: thread t owns the kBins
-    // consecutive entries [kBins*t, kBins*t + kBins) of the flattened array
-    int *flat = &hist[0][0];
-    int vals[kBins];
-    int s = 0;
-#pragma unroll
-    for (int q = 0; q < kBins; ++q) {
-      vals[q] = flat[kBins * t + q];
-      s += vals[q];
-    }
-    int tot;
-    int base = block_excl_scan(s, sh, &tot);
-#pragma unroll
-    for (int q = 0; q < kBins; ++q) {
-      flat[kBins * t + q] = base;
-      base += vals[q];
-    }
-    __syncthreads();
-    for (int64_t x = lo; x < hi; ++x) {
-      const int r = p ? perm_get((p - 1) & 1, x) : (int)x;
-      const int dig = ((nB - lenv(r)) >> shift) & (kBins - 1);
-      perm_put(last, p & 1, hist[dig][t]++, r);
-    }
-    if constexpr (!IN_LDS) __threadfence_block();
-    __syncthreads();
+    return m;
+  };
+  for (int r0 = rlo; r0 < rhi; r0 += 64) {
+    const int r = r0 + lane;
+    if (r < rhi) atomicAdd(&cnt[(nB - lenv(r)) * kWaves + w], 1u);
   }
-  if (passes == 0) {
-    for (int64_t x = lo; x < hi; ++x) order[x] = (int)x;
+  __syncthreads();
+  {
+    // exclusive scan of the counters in index order, a contiguous segment per
+    // thread
+    const int per = (K + kScanThreads - 1) / kScanThreads;
+    const int lo = min(K, per * t), hi = min(K, lo + per);
+    int local = 0;
+    for (int i = lo; i < hi; ++i) local += (int)cnt[i];
+    int total;
+    int run = block_excl_scan(local, sh, &total);
+    for (int i = lo; i < hi; ++i) {
+      const int c = (int)cnt[i];
+      cnt[i] = (uint32_t)run;
+      run += c;
+    }
+  }
+  __syncthreads();
+  for (int r0 = rlo; r0 < rhi; r0 += 64) {
+    const int r = r0 + lane;
+    const bool on = r < rhi;
+    const int L = on ? lenv(r) : 0;
+    const unsigned long long m = peers_of(on, L);
+    if (on) {
+      uint32_t &c = cnt[(nB - L) * kWaves + w];
+      order[(int)c + __popcll(m & ((1ull << lane) - 1ull))] = r;
+      // every lane of the group has read the counter before the lowest lane
+      // writes it back (one wave: its LDS accesses complete in program order)
+      if (lane == __builtin_ctzll(m)) c += (uint32_t)__popcll(m);
+    }
   }
 }
 
@@ -219,27 +237,28 @@ hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows
   return hipGetLastError();
 }
 
-size_t compact_scratch_bytes(int64_t R) { return 3 * align_up((size_t)R * sizeof(int32_t)); }
+size_t compact_scratch_bytes(int64_t R) { return align_up((size_t)R * sizeof(int32_t)); }
 
 hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_ptr,
                           int32_t *col_idx, int32_t *order, void *scratch, hipStream_t s) {
-  char *ws = static_cast<char *>(scratch);
-  const size_t part = align_up((size_t)R * sizeof(int32_t));
-  int32_t *len = reinterpret_cast<int32_t *>(ws);
-  int32_t *tmp0 = reinterpret_cast<int32_t *>(ws + part);
-  int32_t *tmp1 = reinterpret_cast<int32_t *>(ws + 2 * part);
+  int32_t *len = static_cast<int32_t *>(scratch);
   const unsigned g = (unsigned)((R + 3) / 4);
   hipLaunchKernelGGL(count_kernel, dim3(g), dim3(256), 0, s, mask, R, nB, len);
-  if (R <= kLdsRows) {
-    const size_t lds = (size_t)3 * R * sizeof(int32_t);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&scan_sort_kernel<true>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  const size_t cnt_lds = (size_t)(nB + 1) * (kScanThreads / 64) * sizeof(uint32_t);
+  const size_t len_lds = (size_t)R * sizeof(uint16_t);
+  hipError_t e;
+  if (cnt_lds + len_lds <= kCountSortLds) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void *>(&count_sort_kernel<true>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)(cnt_lds + len_lds));
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(scan_sort_kernel<true>, dim3(1), dim3(kScanThreads), lds, s, len, R, nB,
-                       row_ptr, order, tmp0, tmp1);
+    hipLaunchKernelGGL(count_sort_kernel<true>, dim3(1), dim3(kScanThreads), cnt_lds + len_lds, s,
+                       len, (int)R, nB, row_ptr, order);
   } else {
-    hipLaunchKernelGGL(scan_sort_kernel<false>, dim3(1), dim3(kScanThreads), 0, s, len, R, nB,
-                       row_ptr, order, tmp0, tmp1);
+    e = hipFuncSetAttribute(reinterpret_cast<const void *>(&count_sort_kernel<false>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)cnt_lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(count_sort_kernel<false>, dim3(1), dim3(kScanThreads), cnt_lds, s, len,
+                       (int)R, nB, row_ptr, order);
   }
   hipLaunchKernelGGL(fill_kernel, dim3(g), dim3(256), 0, s, mask, R, nB, row_ptr, col_idx);
   return hipGetLastError();

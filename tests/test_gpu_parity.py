@@ -155,10 +155,13 @@ def test_merge_bit_exact(wid):
     np.testing.assert_array_equal(got, oracle.merge_target_rows(m, rows, cols))
 
 
-# R = 5 nb rows: up to 8192 rows the sort runs in LDS, beyond it in HBM
-@pytest.mark.parametrize("nb,density", [(3, 0.5), (139, 0.3), (256, 0.2), (931, 0.1), (2048, 0.05)])
-def test_compaction_bit_exact(nb, density):
-    m = synth.random_mask(1, 5, nb, density, nb)
+# R = heads * nb rows.  The sort keeps its counters in LDS and the row lengths
+# beside them while 64 (nb + 1) + 2 R bytes fit in 152 KiB: (2048, 7) reads
+# the lengths from memory instead.
+@pytest.mark.parametrize("nb,density,heads", [(3, 0.5, 5), (139, 0.3, 5), (256, 0.2, 5), (931, 0.1, 5),
+                                              (2048, 0.05, 5), (2048, 0.05, 7)])
+def test_compaction_bit_exact(nb, density, heads):
+    m = synth.random_mask(1, heads, nb, density, nb)
     m[0, 1, 0] = 0
     m[0, 2, 1] = 1
     dm = torch.as_tensor(m, device=DEV)
