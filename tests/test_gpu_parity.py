@@ -159,7 +159,9 @@ def test_merge_bit_exact(wid):
 # beside them while 64 (nb + 1) + 2 R bytes fit in 152 KiB: (2048, 7) reads
 # the lengths from memory instead.
 @pytest.mark.parametrize("nb,density,heads", [(3, 0.5, 5), (139, 0.3, 5), (256, 0.2, 5), (931, 0.1, 5),
-                                              (2048, 0.05, 5), (2048, 0.05, 7)])
+                                              (2048, 0.05, 5), (2048, 0.05, 7),
+                                              # every row full but one: one length group in row order
+                                              (64, 1.0, 3)])
 def test_compaction_bit_exact(nb, density, heads):
     m = synth.random_mask(1, heads, nb, density, nb)
     m[0, 1, 0] = 0
