@@ -132,8 +132,12 @@ struct Cfg {
 // rescaled at the start of the next iteration, since the P.V in flight in
 // this one still belongs to the old max.  This keeps the softmax free of
 // branches, so it shares one scheduling region with the MFMAs.
+// At d = 64 the non-LSE kernel is held to 168 registers (a few spills), so
+// three workgroups share a CU (their LDS, 3 x 40 KB, fits): with half the
+// MFMAs per score of d = 128 it is bound by its vector work, which a third
+// wave per SIMD overlaps better (2-3 % on the CogVideoX shape).
 template <int D, int BS, bool WITH_LSE>
-__global__ void __launch_bounds__(2 * BS, 2)
+__global__ void __launch_bounds__(2 * BS, (D == 64 && !WITH_LSE) ? 3 : 2)
 bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, int64_t osh,
               int64_t osn, int H, int N, int nB, const int32_t *__restrict__ row_ptr,
               const int32_t *__restrict__ col_idx, const int32_t *__restrict__ order, float c2,
