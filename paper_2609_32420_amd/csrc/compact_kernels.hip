@@ -29,35 +29,49 @@ __global__ void __launch_bounds__(256) merge_kernel(uint8_t *__restrict__ mask, 
   mask[x] = keep ? 1 : 0;
 }
 
+// A row's mask bytes, lane l holding columns l, l + 64, ... (NC of them, at
+// least ceil(nB / 64)).  The column index is clamped to the row rather than
+// the load predicated, so all loads are issued before any is used and a row
+// costs one memory round trip; columns past nB then read as 0.
+template <int NC>
+__device__ inline void load_row(const uint8_t *row, int nB, int lane, uint8_t (&v)[NC]) {
+#pragma unroll
+  for (int c = 0; c < NC; ++c) v[c] = row[min(c * 64 + lane, nB - 1)];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) v[c] = c * 64 + lane < nB ? v[c] : 0;
+}
+
 // One wave per row: number of kept key blocks.
+template <int NC>
 __global__ void __launch_bounds__(256) count_kernel(const uint8_t *__restrict__ mask, int64_t R,
                                                     int nB, int32_t *__restrict__ len) {
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (r >= R) return;
-  const uint8_t *row = mask + r * nB;
+  uint8_t v[NC];
+  load_row(mask + r * nB, nB, lane, v);
   int n = 0;
-  for (int base = 0; base < nB; base += 64) {
-    const int j = base + lane;
-    n += __popcll(__ballot(j < nB && row[j] != 0));
-  }
+#pragma unroll
+  for (int c = 0; c < NC; ++c) n += __popcll(__ballot(v[c] != 0));
   if (lane == 0) len[r] = n;
 }
 
 // One wave per row: ascending kept key blocks at col_idx[row_ptr[r] ...].
+template <int NC>
 __global__ void __launch_bounds__(256) fill_kernel(const uint8_t *__restrict__ mask, int64_t R,
                                                    int nB, const int32_t *__restrict__ row_ptr,
                                                    int32_t *__restrict__ col_idx) {
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (r >= R) return;
-  const uint8_t *row = mask + r * nB;
+  uint8_t v[NC];
+  load_row(mask + r * nB, nB, lane, v);
   int pos = row_ptr[r];
-  for (int base = 0; base < nB; base += 64) {
-    const int j = base + lane;
-    const bool kept = j < nB && row[j] != 0;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const bool kept = v[c] != 0;
     const unsigned long long bits = __ballot(kept);
-    if (kept) col_idx[pos + __popcll(bits & ((1ull << lane) - 1ull))] = j;
+    if (kept) col_idx[pos + __popcll(bits & ((1ull << lane) - 1ull))] = c * 64 + lane;
     pos += __popcll(bits);
   }
 }
@@ -243,7 +257,15 @@ hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_p
                           int32_t *col_idx, int32_t *order, void *scratch, hipStream_t s) {
   int32_t *len = static_cast<int32_t *>(scratch);
   const unsigned g = (unsigned)((R + 3) / 4);
-  hipLaunchKernelGGL(count_kernel, dim3(g), dim3(256), 0, s, mask, R, nB, len);
+  const int nc = (nB + 63) / 64;  // nB <= 2048
+#define CARNATOR_ROWS(KERNEL, ...)                                                         \
+  do {                                                                                   \
+    if (nc <= 4) hipLaunchKernelGGL(KERNEL<4>, dim3(g), dim3(256), 0, s, __VA_ARGS__);   \
+    else if (nc <= 8) hipLaunchKernelGGL(KERNEL<8>, dim3(g), dim3(256), 0, s, __VA_ARGS__); \
+    else if (nc <= 16) hipLaunchKernelGGL(KERNEL<16>, dim3(g), dim3(256), 0, s, __VA_ARGS__); \
+    else hipLaunchKernelGGL(KERNEL<32>, dim3(g), dim3(256), 0, s, __VA_ARGS__);          \
+  } while (0)
+  CARNATOR_ROWS(count_kernel, mask, R, nB, len);
   const size_t cnt_lds = (size_t)(nB + 1) * (kScanThreads / 64) * sizeof(uint32_t);
   const size_t len_lds = (size_t)R * sizeof(uint16_t);
   hipError_t e;
@@ -260,7 +282,8 @@ hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_p
     hipLaunchKernelGGL(count_sort_kernel<false>, dim3(1), dim3(kScanThreads), cnt_lds, s, len,
                        (int)R, nB, row_ptr, order);
   }
-  hipLaunchKernelGGL(fill_kernel, dim3(g), dim3(256), 0, s, mask, R, nB, row_ptr, col_idx);
+  CARNATOR_ROWS(fill_kernel, mask, R, nB, row_ptr, col_idx);
+#undef CARNATOR_ROWS
   return hipGetLastError();
 }
 
