@@ -21,6 +21,12 @@ rocprofv3 FETCH_SIZE / WRITE_SIZE passes, scaled by the same counters on a
 copy of known size (paper_2609_32420_amd/measured_traffic.json); it is null
 when the kernel source no longer matches the one those counters were taken
 on.
+
+``mask_bank`` (after the timed region, skipped with --no-bank): the same
+masks in their stored, bit-packed form -- the builder writing a bank slot
+directly, compaction of a slot with the widening applied while reading, and
+packing a uint8 mask -- each timed alone, with a check that the lists equal
+those of the uint8 path.
 """
 import argparse
 import json
@@ -99,6 +105,64 @@ def cpu_baseline(wl, heads: int = 8):
                       "+ 1 signature scan" % (heads, wl.heads, wl.name, wl.n_blocks)}
 
 
+# a request's stored connectivity: denoising steps x guidance branches x layers
+BANK_SLOTS = (50, 2, 30)
+
+
+def bank_pass(P, torch, stream, sets, flags, masks, lists, ws_mask, wl, steps):
+    """The bit-packed mask bank on the same inputs, outside the timed region:
+    the builder writing a bank slot directly, compaction of that slot for the
+    target (widening applied while reading the bits), and packing a uint8
+    mask.  Each call is timed alone between two events; the lists must equal
+    those of the uint8 path on the same masks."""
+    B, H, nb = wl.batch, wl.heads, wl.n_blocks
+    dev = masks[0].device
+    slots = [torch.empty(B, H, nb, P.mask_words(nb), dtype=torch.int64, device=dev) for _ in sets]
+    packed = torch.empty_like(slots[0])
+    ws_cb = P.compact_block_mask_bits_workspace(slots[0])
+    R = B * H * nb
+    lb = (torch.empty(R + 1, dtype=torch.int32, device=dev), torch.empty(R * nb, dtype=torch.int32, device=dev),
+          torch.empty(R, dtype=torch.int32, device=dev))
+    t = {k: [] for k in ("build_bits", "compact_bits", "pack")}
+    same = True
+    for i in range(steps + 1):
+        si = i % len(sets)
+        x = sets[si][0]
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        e[0].record(stream)
+        P.build_block_mask_bits(x["q_hist"], x["k_hist"], wl.block, wl.tau, out=slots[si], workspace=ws_mask)
+        e[1].record(stream)
+        P.compact_block_mask_bits(slots[si], flags[si][0], flags[si][1], trim=False, out=lb, workspace=ws_cb)
+        e[2].record(stream)
+        P.pack_block_mask(masks[si], out=packed)
+        e[3].record(stream)
+        if i == 0:
+            continue  # warm-up
+        for k, (a, b) in zip(t, ((0, 1), (1, 2), (2, 3))):
+            t[k].append((e[a], e[b]))
+        if i <= len(sets):
+            # masks[si] holds the widened uint8 mask of this set and `lists`
+            # its compaction from the last step of the per-call pass
+            P.compact_block_mask(masks[si], trim=False, out=lists)
+            nnz = int(lists[0][-1].item())
+            same &= bool(torch.equal(lists[0], lb[0]) and torch.equal(lists[2], lb[2])
+                         and torch.equal(lists[1][:nnz], lb[1][:nnz]))
+    torch.cuda.synchronize()
+    ms = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) for k, v in t.items()}
+    slot_bytes = slots[0].numel() * 8
+    return {
+        "layout": "uint64 [B, H, nB, ceil(nB/64)] per (step, branch, layer)",
+        "slot_bytes": slot_bytes,
+        "slot_bytes_uint8": B * H * nb * nb,
+        "request_bank_MB": round(slot_bytes * int(np.prod(BANK_SLOTS)) / 1e6, 1),
+        "request_bank_slots": list(BANK_SLOTS),
+        "build_bits_ms_per_call": round(ms["build_bits"], 4),
+        "compact_bits_ms_per_call": round(ms["compact_bits"], 4),
+        "pack_ms_per_call": round(ms["pack"], 4),
+        "lists_equal_uint8_path": same,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -107,6 +171,7 @@ def main():
     ap.add_argument("--workload", type=int, default=1)
     ap.add_argument("--sets", type=int, default=3, help="input sets rotated across steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bank", action="store_true", help="skip the bit-packed mask bank pass")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before timing, copy a buffer of this size once (a reference kernel of known "
                          "traffic for hardware byte counters)")
@@ -205,6 +270,9 @@ def main():
     def avg_ms(name):
         return float(np.mean([a.elapsed_time(b) for a, b in ev[name]]))
 
+    bank = None if args.no_bank else bank_pass(P, torch, stream, sets, flags, masks, lists, ws_mask, wl,
+                                                args.steps)
+
     # algorithmic work of one step (averaged over the rotated sets)
     fl_exec = float(np.mean([executed_flops(m.cpu().numpy(), N, bs, d) for m in masks]))
     density = float(np.mean([m.float().mean().item() for m in masks]))
@@ -252,6 +320,8 @@ def main():
                      "traffic": measured_traffic(d, bs),
                      "kernel": "bsattn_kernel<%d, %d> (one launch of carnator_block_sparse_attn_lists)" % (d, bs)},
     }
+    if bank is not None:
+        res["mask_bank"] = bank
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(wl)

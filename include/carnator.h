@@ -10,6 +10,10 @@
  *                               rows (Sec. 3.3, joint reuse in the middle
  *                               layers)
  *   carnator_compact_block_mask per-row lists of kept key blocks
+ *   carnator_*_bits, carnator_pack_block_mask, carnator_unpack_block_mask
+ *                               the same masks bit-packed, the form in which
+ *                               the historical connectivity is stored and
+ *                               reused (Sec. 3.3, Appendix C.3)
  *   carnator_block_sparse_attn  attention of the recomputed target Q, K, V
  *                               under the reused structure (Sec. 3.3,
  *                               historical sparse-connectivity reuse)
@@ -43,6 +47,12 @@
  *   read or written.
  * - Block masks are uint8 [B, H, nB, nB], contiguous; 0 drops a block pair,
  *   any other byte keeps it.  The builder writes exactly 0 or 1.
+ * - Bit-packed block masks are uint64 [B, H, nB, W], W = ceil(nB / 64),
+ *   contiguous, 8-byte aligned: key block j of row (b, h, i) is bit j mod 64
+ *   (least significant first) of word j / 64 of that row.  Bits j >= nB of
+ *   a row's last word are written as 0 and ignored when read.  A bank of
+ *   masks over S denoising steps, C branches and L layers is one array
+ *   [S, C, L, B, H, nB, W]; each slot is a mask of this layout.
  * - Supported: head_dim in {64, 128}, block in {64, 128}.  Anything else
  *   returns CARNATOR_E_UNSUPPORTED.
  */
@@ -57,7 +67,7 @@
 extern "C" {
 #endif
 
-#define CARNATOR_ABI_VERSION 1
+#define CARNATOR_ABI_VERSION 2
 
 typedef enum {
   CARNATOR_OK = 0,
@@ -156,6 +166,53 @@ size_t carnator_compact_block_mask_workspace_size(const carnator_shape *shape);
 int carnator_compact_block_mask(const uint8_t *mask, const carnator_shape *shape,
                                 int32_t *row_ptr, int32_t *col_idx, int32_t *order,
                                 void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Bit-packed masks: the historical block connectivity in its stored form.
+ * The paper keeps the sparse connectivity of the historical run per
+ * denoising step, branch, layer and head and reuses it for later requests
+ * (Sec. 3.3, Appendix C.3); one bit per block pair is an eighth of the
+ * uint8 mask.  Layout: see "Bit-packed block masks" above.
+ *
+ * carnator_build_block_mask_bits: carnator_build_block_mask with the mask
+ * written bit-packed (same arguments, same workspace size, the same decisions
+ * bit for bit).
+ *   bits_out  uint64 [B, H, nB, W]
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_WORKSPACE, E_HIP.
+ *
+ * carnator_pack_block_mask: bits[b,h,i] bit j = (mask[b,h,i,j] != 0).
+ * carnator_unpack_block_mask: mask[b,h,i,j] = bit j of bits[b,h,i] as 0/1
+ * bytes.
+ *   mask  uint8 [B, H, nB, nB]; bits uint64 [B, H, nB, W]
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_HIP.
+ *
+ * carnator_compact_block_mask_bits: the lists carnator_compact_block_mask
+ * writes for the mask carnator_merge_target_rows would make of the unpacked
+ * bits (same row_ptr, col_idx and order), computed from the words directly;
+ * the bits are only read, so one stored mask serves any target.
+ *   bits         uint64 [B, H, nB, W]
+ *   target_rows  uint8 [B, nB] or NULL; nonzero widens query block i to a
+ *                full row
+ *   dense_cols   uint8 [B, nB] or NULL; nonzero keeps key block j in every
+ *                row
+ *   row_ptr, col_idx, order: as carnator_compact_block_mask
+ *   workspace    at least carnator_compact_block_mask_bits_workspace_size
+ *                (shape) bytes, 256-byte aligned
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_WORKSPACE, E_HIP.
+ */
+int carnator_build_block_mask_bits(const carnator_view *q_hist, const carnator_view *k_hist,
+                                   const carnator_shape *shape, float scale,
+                                   double mass_threshold, uint64_t *bits_out, void *workspace,
+                                   size_t workspace_bytes, hipStream_t stream);
+int carnator_pack_block_mask(const uint8_t *mask, const carnator_shape *shape, uint64_t *bits,
+                             hipStream_t stream);
+int carnator_unpack_block_mask(const uint64_t *bits, const carnator_shape *shape, uint8_t *mask,
+                               hipStream_t stream);
+size_t carnator_compact_block_mask_bits_workspace_size(const carnator_shape *shape);
+int carnator_compact_block_mask_bits(const uint64_t *bits, const carnator_shape *shape,
+                                     const uint8_t *target_rows, const uint8_t *dense_cols,
+                                     int32_t *row_ptr, int32_t *col_idx, int32_t *order,
+                                     void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Block-sparse attention -- Sec. 3.3 ("Historical Sparse-Connectivity

@@ -18,6 +18,8 @@ Every function is plain fp64 NumPy, written from the paper's definitions:
   is preserved for the active region).
 * ``compact_mask``: the per-row list of kept key blocks that the sparse
   executor walks.
+* ``pack_mask`` / ``unpack_mask``: the masks as one bit per block pair, the
+  form in which they are stored per step, branch and layer (Appendix C.3).
 * ``block_sparse_attention``: softmax attention of the recomputed target
   Q, K, V restricted to the reused block structure (Sec. 3.3, "Historical
   Sparse-Connectivity Reuse"; Appendix C.3).
@@ -30,7 +32,7 @@ of each submodule.
 """
 from .mask import (pool_blocks, block_scores, select_row, build_block_mask,
                    merge_target_rows, compact_mask, row_admissible_masks, TIE_EPS,
-                   FRAGILE_EPS)
+                   FRAGILE_EPS, pack_mask, unpack_mask)
 from .attention import block_sparse_attention, token_mask_from_blocks
 from .cosine import cosine_similarity, topk_cosine
 from .convert import to_f64
@@ -38,6 +40,6 @@ from .convert import to_f64
 __all__ = [
     "pool_blocks", "block_scores", "select_row", "build_block_mask",
     "merge_target_rows", "compact_mask", "row_admissible_masks", "TIE_EPS",
-    "FRAGILE_EPS", "block_sparse_attention", "token_mask_from_blocks",
+    "FRAGILE_EPS", "pack_mask", "unpack_mask", "block_sparse_attention", "token_mask_from_blocks",
     "cosine_similarity", "topk_cosine", "to_f64",
 ]

@@ -25,6 +25,10 @@ Readings (the paper is silent on these points):
    one the sorted prefix gives).
 5. Target widening: a flagged query block becomes a full row; a flagged key
    block (dense text columns) becomes a full column.
+6. Stored form: the paper keeps the binary masks but names no encoding.  One
+   bit per block pair, key block j of a row at bit j mod 64 (least
+   significant first) of the row's 64-bit word j // 64, unused high bits of
+   the last word zero.
 """
 import numpy as np
 
@@ -165,3 +169,28 @@ def compact_mask(mask: np.ndarray):
     col_idx = np.nonzero(flat)[1]
     order = np.argsort(-counts, kind="stable")
     return row_ptr.astype(np.int32), col_idx.astype(np.int32), order.astype(np.int32)
+
+
+def pack_mask(mask: np.ndarray) -> np.ndarray:
+    """Bit-packed form of a block mask [..., nB, nB]: uint64 [..., nB, W],
+    W = ceil(nB / 64); word w of a row holds key blocks 64 w .. 64 w + 63,
+    block j at bit j - 64 w.  Bits past nB are 0."""
+    m = (np.asarray(mask) != 0)
+    nb = m.shape[-1]
+    w = (nb + 63) // 64
+    padded = np.zeros(m.shape[:-1] + (w * 64,), dtype=np.uint64)
+    padded[..., :nb] = m
+    chunks = padded.reshape(m.shape[:-1] + (w, 64))
+    weights = np.left_shift(np.uint64(1), np.arange(64, dtype=np.uint64))
+    # distinct powers of two: the sum is the bitwise OR
+    return (chunks * weights).sum(axis=-1, dtype=np.uint64)
+
+
+def unpack_mask(bits: np.ndarray, nb: int) -> np.ndarray:
+    """Inverse of pack_mask: 0/1 bytes [..., nB, nB]; bits past nB are
+    ignored."""
+    b = np.asarray(bits, dtype=np.uint64)
+    shifts = np.arange(64, dtype=np.uint64)
+    cols = (b[..., :, None] >> shifts) & np.uint64(1)
+    flat = cols.reshape(b.shape[:-1] + (b.shape[-1] * 64,))
+    return flat[..., :nb].astype(np.uint8)

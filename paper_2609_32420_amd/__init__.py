@@ -18,6 +18,8 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libcarnator.so")
 
 CARNATOR_OK = 0
+# CARNATOR_ABI_VERSION of include/carnator.h this binding marshals for
+ABI_VERSION = 2
 STATUS = {0: "OK", -1: "E_NULL", -2: "E_SHAPE", -3: "E_UNSUPPORTED", -4: "E_ALIGN",
           -5: "E_WORKSPACE", -6: "E_HIP"}
 
@@ -27,6 +29,8 @@ EXPORTS = (
     "carnator_build_block_mask_workspace_size", "carnator_build_block_mask",
     "carnator_merge_target_rows",
     "carnator_compact_block_mask_workspace_size", "carnator_compact_block_mask",
+    "carnator_build_block_mask_bits", "carnator_pack_block_mask", "carnator_unpack_block_mask",
+    "carnator_compact_block_mask_bits_workspace_size", "carnator_compact_block_mask_bits",
     "carnator_block_sparse_attn_workspace_size", "carnator_block_sparse_attn",
     "carnator_block_sparse_attn_lists",
     "carnator_signature_sim_workspace_size", "carnator_signature_sim",
@@ -71,6 +75,11 @@ def lib() -> ctypes.CDLL:
             "carnator_merge_target_rows": (ctypes.c_int, [P, SP, P, P, P]),
             "carnator_compact_block_mask_workspace_size": (SZ, [SP]),
             "carnator_compact_block_mask": (ctypes.c_int, [P, SP, P, P, P, P, SZ, P]),
+            "carnator_build_block_mask_bits": (ctypes.c_int, [VP, VP, SP, F32, F64, P, P, SZ, P]),
+            "carnator_pack_block_mask": (ctypes.c_int, [P, SP, P, P]),
+            "carnator_unpack_block_mask": (ctypes.c_int, [P, SP, P, P]),
+            "carnator_compact_block_mask_bits_workspace_size": (SZ, [SP]),
+            "carnator_compact_block_mask_bits": (ctypes.c_int, [P, SP, P, P, P, P, P, P, SZ, P]),
             "carnator_block_sparse_attn_workspace_size": (SZ, [SP]),
             "carnator_block_sparse_attn": (ctypes.c_int, [VP, VP, VP, P, I64, I64, I64, SP, P, F32, P, P,
                                                           SZ, P]),
@@ -83,6 +92,9 @@ def lib() -> ctypes.CDLL:
             f = getattr(L, name)
             f.restype = res
             f.argtypes = args
+        if L.carnator_abi_version() != ABI_VERSION:
+            raise RuntimeError("libcarnator.so has ABI version %d, the binding expects %d (rebuild it)"
+                               % (L.carnator_abi_version(), ABI_VERSION))
         _lib = L
     return _lib
 
@@ -207,6 +219,147 @@ def compact_block_mask(mask: torch.Tensor, trim: bool = True, out=None,
         nnz = int(row_ptr[-1].item())
         return row_ptr, col_idx[:nnz], order
     return row_ptr, col_idx, order
+
+
+# ---------------------------------------------------------------- bit-packed masks
+#
+# A packed mask is an int64 tensor [B, H, nB, W], W = ceil(nB / 64), holding
+# the uint64 words of include/carnator.h (torch has no general uint64 device
+# arithmetic; the bits are the same).
+
+
+def mask_words(nb: int) -> int:
+    """Words per packed mask row."""
+    return (nb + 63) // 64
+
+
+def _bits_shape(bits: torch.Tensor):
+    if bits.dim() != 4 or bits.dtype != torch.int64 or not bits.is_contiguous():
+        raise ValueError("bits must be a contiguous int64 [B, H, nB, W] tensor")
+    B, H, nb, w = bits.shape
+    if w != mask_words(nb):
+        raise ValueError("bits has %d words per row; nB = %d needs %d" % (w, nb, mask_words(nb)))
+    return B, H, nb
+
+
+def build_block_mask_bits(q_hist: torch.Tensor, k_hist: torch.Tensor, block: int, mass_threshold: float,
+                          scale: float = 0.0, out: Optional[torch.Tensor] = None,
+                          workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Historical block mask, bit-packed: int64 [B, H, nB, W]
+    (carnator_build_block_mask_bits)."""
+    s = _shape(q_hist, block)
+    if tuple(k_hist.shape) != tuple(q_hist.shape):
+        raise ValueError("q_hist and k_hist shapes differ")
+    nb = -(-s.seq_len // block)
+    if out is None:
+        out = torch.empty(s.batch, s.heads, nb, mask_words(nb), dtype=torch.int64, device=q_hist.device)
+    elif tuple(out.shape) != (s.batch, s.heads, nb, mask_words(nb)):
+        raise ValueError("out must have shape %s" % ((s.batch, s.heads, nb, mask_words(nb)),))
+    _bits_shape(out)
+    L = lib()
+    ws = workspace if workspace is not None else build_block_mask_workspace(q_hist, block)
+    qv, kv = _view(q_hist), _view(k_hist)
+    _check(L.carnator_build_block_mask_bits(ctypes.byref(qv), ctypes.byref(kv), ctypes.byref(s), float(scale),
+                                            float(mass_threshold), _ptr(out), _ptr(ws), ws.numel(),
+                                            _stream(q_hist)))
+    return out
+
+
+def pack_block_mask(mask: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """uint8 [B, H, nB, nB] -> packed int64 [B, H, nB, W]."""
+    B, H, nb, nb2 = mask.shape
+    if mask.dtype != torch.uint8 or not mask.is_contiguous() or nb != nb2:
+        raise ValueError("mask must be a contiguous uint8 [B, H, nB, nB] tensor")
+    if out is None:
+        out = torch.empty(B, H, nb, mask_words(nb), dtype=torch.int64, device=mask.device)
+    if _bits_shape(out) != (B, H, nb):
+        raise ValueError("out must have shape %s" % ((B, H, nb, mask_words(nb)),))
+    s = Shape(B, H, nb * 64, 64, 64)
+    _check(lib().carnator_pack_block_mask(_ptr(mask), ctypes.byref(s), _ptr(out), _stream(mask)))
+    return out
+
+
+def unpack_block_mask(bits: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Packed int64 [B, H, nB, W] -> uint8 [B, H, nB, nB] of 0/1."""
+    B, H, nb = _bits_shape(bits)
+    if out is None:
+        out = torch.empty(B, H, nb, nb, dtype=torch.uint8, device=bits.device)
+    if out.dtype != torch.uint8 or not out.is_contiguous() or tuple(out.shape) != (B, H, nb, nb):
+        raise ValueError("out must be a contiguous uint8 %s tensor" % ((B, H, nb, nb),))
+    s = Shape(B, H, nb * 64, 64, 64)
+    _check(lib().carnator_unpack_block_mask(_ptr(bits), ctypes.byref(s), _ptr(out), _stream(bits)))
+    return out
+
+
+def compact_block_mask_bits_workspace(bits: torch.Tensor) -> torch.Tensor:
+    B, H, nb = _bits_shape(bits)
+    s = Shape(B, H, nb * 64, 64, 64)
+    return _workspace(lib().carnator_compact_block_mask_bits_workspace_size(ctypes.byref(s)), bits.device)
+
+
+def compact_block_mask_bits(bits: torch.Tensor, target_rows=None, dense_cols=None, trim: bool = True,
+                            out=None, workspace: Optional[torch.Tensor] = None):
+    """(row_ptr, col_idx, order) of the packed mask widened by target_rows and
+    dense_cols (each [B, nB] or None); the bits are not modified.  trim and out
+    as in compact_block_mask."""
+    B, H, nb = _bits_shape(bits)
+    R = B * H * nb
+    dev = bits.device
+    rows = _dev_u8(target_rows, dev, (B, nb))
+    cols = _dev_u8(dense_cols, dev, (B, nb))
+    s = Shape(B, H, nb * 64, 64, 64)
+    if out is None:
+        out = (torch.empty(R + 1, dtype=torch.int32, device=dev),
+               torch.empty(max(R * nb, 1), dtype=torch.int32, device=dev),
+               torch.empty(R, dtype=torch.int32, device=dev))
+    row_ptr, col_idx, order = out
+    if row_ptr.numel() < R + 1 or col_idx.numel() < R * nb or order.numel() < R:
+        raise ValueError("out tensors too small")
+    if workspace is None:
+        workspace = compact_block_mask_bits_workspace(bits)
+    _check(lib().carnator_compact_block_mask_bits(_ptr(bits), ctypes.byref(s), _ptr(rows), _ptr(cols),
+                                                  _ptr(row_ptr), _ptr(col_idx), _ptr(order), _ptr(workspace),
+                                                  workspace.numel(), _stream(bits)))
+    if trim:
+        nnz = int(row_ptr[-1].item())
+        return row_ptr, col_idx[:nnz], order
+    return row_ptr, col_idx, order
+
+
+class MaskBank:
+    """The reused connectivity of one historical request: a packed block mask
+    per (denoising step, guidance branch, layer), each [B, H, nB, W], in one
+    int64 array [steps, branches, layers, B, H, nB, W] on the device."""
+
+    def __init__(self, steps: int, branches: int, layers: int, batch: int, heads: int, n_blocks: int,
+                 device="cuda"):
+        self.n_blocks = n_blocks
+        self.bits = torch.zeros(steps, branches, layers, batch, heads, n_blocks, mask_words(n_blocks),
+                                dtype=torch.int64, device=device)
+
+    @property
+    def nbytes(self) -> int:
+        return self.bits.numel() * 8
+
+    def slot(self, step: int, branch: int, layer: int) -> torch.Tensor:
+        return self.bits[step, branch, layer]
+
+    def record(self, step: int, branch: int, layer: int, q_hist: torch.Tensor, k_hist: torch.Tensor,
+               block: int, mass_threshold: float, scale: float = 0.0,
+               workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """Builds the historical mask of one slot straight into the bank."""
+        return build_block_mask_bits(q_hist, k_hist, block, mass_threshold, scale,
+                                     out=self.slot(step, branch, layer), workspace=workspace)
+
+    def store(self, step: int, branch: int, layer: int, mask: torch.Tensor) -> torch.Tensor:
+        """Packs a uint8 mask into one slot."""
+        return pack_block_mask(mask, out=self.slot(step, branch, layer))
+
+    def lists(self, step: int, branch: int, layer: int, target_rows=None, dense_cols=None,
+              trim: bool = True, out=None, workspace: Optional[torch.Tensor] = None):
+        """Compacted lists of one slot for a target (compact_block_mask_bits)."""
+        return compact_block_mask_bits(self.slot(step, branch, layer), target_rows, dense_cols, trim=trim,
+                                       out=out, workspace=workspace)
 
 
 def block_sparse_attn_workspace(q: torch.Tensor, block: int) -> torch.Tensor:

@@ -129,23 +129,27 @@ size_t carnator_build_block_mask_workspace_size(const carnator_shape *s) {
   return 2 * per;
 }
 
-int carnator_build_block_mask(const carnator_view *q_hist, const carnator_view *k_hist,
-                              const carnator_shape *s, float scale, double mass_threshold,
-                              uint8_t *mask_out, void *workspace, size_t ws_bytes,
-                              hipStream_t stream) {
+// The builder behind both output forms: exactly one of mask_out and bits_out
+// is non-NULL.
+static int build_mask(const carnator_view *q_hist, const carnator_view *k_hist,
+                      const carnator_shape *s, float scale, double mass_threshold,
+                      uint8_t *mask_out, uint64_t *bits_out, void *workspace, size_t ws_bytes,
+                      hipStream_t stream) {
   int rc;
   if ((rc = check_shape(s))) return rc;
   if ((rc = check_view(q_hist, s, "q_hist"))) return rc;
   if ((rc = check_view(k_hist, s, "k_hist"))) return rc;
-  if (!mask_out) return fail(CARNATOR_E_NULL, "mask_out is NULL");
+  if (!mask_out && !bits_out) return fail(CARNATOR_E_NULL, "the output is NULL");
+  if (bits_out && reinterpret_cast<uintptr_t>(bits_out) % 8 != 0)
+    return fail(CARNATOR_E_ALIGN, "bits_out must be 8-byte aligned");
   if (!(mass_threshold > 0.0)) return fail(CARNATOR_E_SHAPE, "mass_threshold must be > 0");
   if (!isfinite(scale)) return fail(CARNATOR_E_SHAPE, "scale must be finite");
   const int nB = n_blocks(s);
   const int BH = s->batch * s->heads;
-  const size_t mask_bytes = (size_t)BH * nB * nB;
   if (mass_threshold >= 1.0) {
     // every block pair is kept; no workspace is touched
-    hipError_t e = launch_fill_ones(mask_out, mask_bytes, stream);
+    hipError_t e = bits_out ? launch_fill_ones_bits(bits_out, (int64_t)BH * nB, nB, stream)
+                            : launch_fill_ones(mask_out, (size_t)BH * nB * nB, stream);
     if (e != hipSuccess) return hip_fail(e, "fill");
     return ok();
   }
@@ -158,9 +162,28 @@ int carnator_build_block_mask(const carnator_view *q_hist, const carnator_view *
   hipError_t e = launch_pool(to_view(q_hist), to_view(k_hist), s->batch, s->heads, s->seq_len,
                              s->head_dim, s->block, qbar, kbar, stream);
   if (e != hipSuccess) return hip_fail(e, "pool");
-  e = launch_select(qbar, kbar, BH, nB, s->head_dim, sigma, mass_threshold, mask_out, stream);
+  e = launch_select(qbar, kbar, BH, nB, s->head_dim, sigma, mass_threshold, mask_out, bits_out,
+                    stream);
   if (e != hipSuccess) return hip_fail(e, "select");
   return ok();
+}
+
+int carnator_build_block_mask(const carnator_view *q_hist, const carnator_view *k_hist,
+                              const carnator_shape *s, float scale, double mass_threshold,
+                              uint8_t *mask_out, void *workspace, size_t ws_bytes,
+                              hipStream_t stream) {
+  if (!mask_out) return fail(CARNATOR_E_NULL, "mask_out is NULL");
+  return build_mask(q_hist, k_hist, s, scale, mass_threshold, mask_out, nullptr, workspace,
+                    ws_bytes, stream);
+}
+
+int carnator_build_block_mask_bits(const carnator_view *q_hist, const carnator_view *k_hist,
+                                   const carnator_shape *s, float scale, double mass_threshold,
+                                   uint64_t *bits_out, void *workspace, size_t ws_bytes,
+                                   hipStream_t stream) {
+  if (!bits_out) return fail(CARNATOR_E_NULL, "bits_out is NULL");
+  return build_mask(q_hist, k_hist, s, scale, mass_threshold, nullptr, bits_out, workspace,
+                    ws_bytes, stream);
 }
 
 // ---------------------------------------------------------------- merge
@@ -195,6 +218,58 @@ int carnator_compact_block_mask(const uint8_t *mask, const carnator_shape *s, in
   hipError_t e = launch_compact(mask, (int64_t)s->batch * s->heads * nB, nB, row_ptr, col_idx,
                                 order, workspace, stream);
   if (e != hipSuccess) return hip_fail(e, "compact");
+  return ok();
+}
+
+// ---------------------------------------------------------------- bit-packed masks
+
+int carnator_pack_block_mask(const uint8_t *mask, const carnator_shape *s, uint64_t *bits,
+                             hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if (!mask || !bits) return fail(CARNATOR_E_NULL, "mask and bits must be non-NULL");
+  if (reinterpret_cast<uintptr_t>(bits) % 8 != 0)
+    return fail(CARNATOR_E_ALIGN, "bits must be 8-byte aligned");
+  const int nB = n_blocks(s);
+  hipError_t e = launch_pack(mask, (int64_t)s->batch * s->heads * nB, nB, bits, stream);
+  if (e != hipSuccess) return hip_fail(e, "pack");
+  return ok();
+}
+
+int carnator_unpack_block_mask(const uint64_t *bits, const carnator_shape *s, uint8_t *mask,
+                               hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if (!mask || !bits) return fail(CARNATOR_E_NULL, "bits and mask must be non-NULL");
+  if (reinterpret_cast<uintptr_t>(bits) % 8 != 0)
+    return fail(CARNATOR_E_ALIGN, "bits must be 8-byte aligned");
+  const int nB = n_blocks(s);
+  hipError_t e = launch_unpack(bits, (int64_t)s->batch * s->heads * nB, nB, mask, stream);
+  if (e != hipSuccess) return hip_fail(e, "unpack");
+  return ok();
+}
+
+size_t carnator_compact_block_mask_bits_workspace_size(const carnator_shape *s) {
+  if (check_shape(s) != CARNATOR_OK) return 0;
+  return compact_bits_scratch_bytes((int64_t)s->batch * s->heads * n_blocks(s), s->batch,
+                                    n_blocks(s));
+}
+
+int carnator_compact_block_mask_bits(const uint64_t *bits, const carnator_shape *s,
+                                     const uint8_t *target_rows, const uint8_t *dense_cols,
+                                     int32_t *row_ptr, int32_t *col_idx, int32_t *order,
+                                     void *workspace, size_t ws_bytes, hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if (!bits || !row_ptr || !col_idx || !order)
+    return fail(CARNATOR_E_NULL, "bits, row_ptr, col_idx and order must be non-NULL");
+  if (reinterpret_cast<uintptr_t>(bits) % 8 != 0)
+    return fail(CARNATOR_E_ALIGN, "bits must be 8-byte aligned");
+  if ((rc = check_ws(workspace, ws_bytes, carnator_compact_block_mask_bits_workspace_size(s))))
+    return rc;
+  hipError_t e = launch_compact_bits(bits, s->batch, s->heads, n_blocks(s), target_rows,
+                                     dense_cols, row_ptr, col_idx, order, workspace, stream);
+  if (e != hipSuccess) return hip_fail(e, "compact_bits");
   return ok();
 }
 

@@ -1,5 +1,5 @@
 // Target-row widening of the reused mask and its compaction into per-row
-// lists of kept key blocks.
+// lists of kept key blocks, from the uint8 mask or from its bit-packed form.
 //
 // Widening (Sec. 3.3, joint reuse in the middle layers): a target-specific
 // query block evaluates every key block, and dense text key blocks are kept
@@ -7,6 +7,12 @@
 // row_ptr / col_idx (ascending key blocks per row) and an order of rows by
 // descending list length (lower row first on equal length), so the longest
 // rows start first.
+//
+// Bit-packed masks (the stored form of the reused connectivity, one bit per
+// block pair): uint64 [rows][nw], nw = ceil(nB / 64), key block j of a row
+// at bit j mod 64 of word j / 64; bits past nB are written as 0 and ignored
+// when read.  Compaction from bits applies the widening while it reads the
+// words, so a stored mask is never modified.
 #include "internal.h"
 
 namespace carnator {
@@ -73,6 +79,116 @@ __global__ void __launch_bounds__(256) fill_kernel(const uint8_t *__restrict__ m
     const unsigned long long bits = __ballot(kept);
     if (kept) col_idx[pos + __popcll(bits & ((1ull << lane) - 1ull))] = c * 64 + lane;
     pos += __popcll(bits);
+  }
+}
+
+// ---- bit-packed masks
+
+// Valid-column bits of word c of a row (the last word may be partial).
+__device__ inline uint64_t valid_bits(int c, int nB, int nw) {
+  return (c == nw - 1 && (nB & 63)) ? (1ull << (nB & 63)) - 1ull : ~0ull;
+}
+
+// One wave per row of nB bytes: lane c < nw writes word c, the ballot of
+// chunk c's nonzero bytes.
+template <int NC>
+__global__ void __launch_bounds__(256) pack_kernel(const uint8_t *__restrict__ mask, int64_t R,
+                                                   int nB, uint64_t *__restrict__ bits) {
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= R) return;
+  uint8_t v[NC];
+  load_row(mask + r * nB, nB, lane, v);
+  uint64_t mine = 0;
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const uint64_t w = __ballot(v[c] != 0);
+    mine = lane == c ? w : mine;
+  }
+  const int nw = (nB + 63) / 64;
+  if (lane < nw) bits[r * nw + lane] = mine;
+}
+
+// One wave per row: lane c < nw loads word c, then each chunk is broadcast
+// and written as 0/1 bytes, 64 columns per store.
+__global__ void __launch_bounds__(256) unpack_kernel(const uint64_t *__restrict__ bits, int64_t R,
+                                                     int nB, uint8_t *__restrict__ mask) {
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= R) return;
+  const int nw = (nB + 63) / 64;
+  const uint64_t mine = lane < nw ? bits[r * nw + lane] : 0ull;
+  uint8_t *out = mask + r * nB;
+  for (int c = 0; c < nw; ++c) {
+    const uint64_t w = read_lane(mine, c);
+    const int j = c * 64 + lane;
+    if (j < nB) out[j] = (uint8_t)((w >> lane) & 1ull);
+  }
+}
+
+// Every block pair kept: all valid bits set, the rest 0.  One thread per word.
+__global__ void __launch_bounds__(256) fill_ones_bits_kernel(uint64_t *__restrict__ bits,
+                                                             int64_t words, int nB) {
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (x >= words) return;
+  const int nw = (nB + 63) / 64;
+  bits[x] = valid_bits((int)(x % nw), nB, nw);
+}
+
+// Word c of row r after the widening: all valid bits when the row's query
+// block is target-specific, OR the packed dense-column word of its batch
+// entry (colw [B][nw], or NULL).  HnB = H nB rows per batch entry.
+__device__ inline uint64_t merged_word(const uint64_t *__restrict__ bits, int r, int c, int nB,
+                                       int nw, int HnB, const uint8_t *__restrict__ rows,
+                                       const uint64_t *__restrict__ colw) {
+  uint64_t w = bits[(int64_t)r * nw + c];
+  if (rows != nullptr || colw != nullptr) {
+    const int b = r / HnB;
+    if (rows != nullptr && rows[(int64_t)b * nB + r % nB] != 0) w = ~0ull;
+    if (colw != nullptr) w |= colw[(int64_t)b * nw + c];
+  }
+  return w & valid_bits(c, nB, nw);
+}
+
+// G lanes per row (G a power of two >= nw), 64 / G rows per wave: list
+// lengths as popcounts summed over each row's lanes.
+template <int G>
+__global__ void __launch_bounds__(256) count_bits_kernel(const uint64_t *__restrict__ bits, int R,
+                                                         int nB, int HnB,
+                                                         const uint8_t *__restrict__ rows,
+                                                         const uint64_t *__restrict__ colw,
+                                                         int32_t *__restrict__ len) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * (64 / G) + lane / G;
+  const int c = lane % G;
+  const int nw = (nB + 63) / 64;
+  int n = 0;
+  if (r < R && c < nw) n = __popcll(merged_word(bits, (int)r, c, nB, nw, HnB, rows, colw));
+#pragma unroll
+  for (int o = 1; o < G; o <<= 1) n += __shfl_xor(n, o);
+  if (r < R && c == 0) len[r] = n;
+}
+
+// One wave per row: ascending kept key blocks at col_idx[row_ptr[r] ...].
+// Lane c < nw holds word c; chunk c is broadcast and each lane writes its
+// column when its bit is set, at the count of set bits below it.
+__global__ void __launch_bounds__(256) fill_bits_kernel(const uint64_t *__restrict__ bits, int R,
+                                                        int nB, int HnB,
+                                                        const uint8_t *__restrict__ rows,
+                                                        const uint64_t *__restrict__ colw,
+                                                        const int32_t *__restrict__ row_ptr,
+                                                        int32_t *__restrict__ col_idx) {
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= R) return;
+  const int nw = (nB + 63) / 64;
+  const uint64_t mine = lane < nw ? merged_word(bits, (int)r, lane, nB, nw, HnB, rows, colw) : 0ull;
+  const uint64_t below = (1ull << lane) - 1ull;
+  int pos = row_ptr[r];
+  for (int c = 0; c < nw; ++c) {
+    const uint64_t w = read_lane(mine, c);
+    if ((w >> lane) & 1ull) col_idx[pos + __popcll(w & below)] = c * 64 + lane;
+    pos += __popcll(w);
   }
 }
 
@@ -253,19 +369,9 @@ hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows
 
 size_t compact_scratch_bytes(int64_t R) { return align_up((size_t)R * sizeof(int32_t)); }
 
-hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_ptr,
-                          int32_t *col_idx, int32_t *order, void *scratch, hipStream_t s) {
-  int32_t *len = static_cast<int32_t *>(scratch);
-  const unsigned g = (unsigned)((R + 3) / 4);
-  const int nc = (nB + 63) / 64;  // nB <= 2048
-#define CARNATOR_ROWS(KERNEL, ...)                                                         \
-  do {                                                                                   \
-    if (nc <= 4) hipLaunchKernelGGL(KERNEL<4>, dim3(g), dim3(256), 0, s, __VA_ARGS__);   \
-    else if (nc <= 8) hipLaunchKernelGGL(KERNEL<8>, dim3(g), dim3(256), 0, s, __VA_ARGS__); \
-    else if (nc <= 16) hipLaunchKernelGGL(KERNEL<16>, dim3(g), dim3(256), 0, s, __VA_ARGS__); \
-    else hipLaunchKernelGGL(KERNEL<32>, dim3(g), dim3(256), 0, s, __VA_ARGS__);          \
-  } while (0)
-  CARNATOR_ROWS(count_kernel, mask, R, nB, len);
+// row_ptr and order from the list lengths (one workgroup).
+static hipError_t launch_sort(const int32_t *len, int64_t R, int nB, int32_t *row_ptr, int32_t *order,
+                       hipStream_t s) {
   const size_t cnt_lds = (size_t)(nB + 1) * (kScanThreads / 64) * sizeof(uint32_t);
   const size_t len_lds = (size_t)R * sizeof(uint16_t);
   hipError_t e;
@@ -282,8 +388,84 @@ hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_p
     hipLaunchKernelGGL(count_sort_kernel<false>, dim3(1), dim3(kScanThreads), cnt_lds, s, len,
                        (int)R, nB, row_ptr, order);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_ptr,
+                          int32_t *col_idx, int32_t *order, void *scratch, hipStream_t s) {
+  int32_t *len = static_cast<int32_t *>(scratch);
+  const unsigned g = (unsigned)((R + 3) / 4);
+  const int nc = (nB + 63) / 64;  // nB <= 2048
+#define CARNATOR_ROWS(KERNEL, ...)                                                         \
+  do {                                                                                   \
+    if (nc <= 4) hipLaunchKernelGGL(KERNEL<4>, dim3(g), dim3(256), 0, s, __VA_ARGS__);   \
+    else if (nc <= 8) hipLaunchKernelGGL(KERNEL<8>, dim3(g), dim3(256), 0, s, __VA_ARGS__); \
+    else if (nc <= 16) hipLaunchKernelGGL(KERNEL<16>, dim3(g), dim3(256), 0, s, __VA_ARGS__); \
+    else hipLaunchKernelGGL(KERNEL<32>, dim3(g), dim3(256), 0, s, __VA_ARGS__);          \
+  } while (0)
+  CARNATOR_ROWS(count_kernel, mask, R, nB, len);
+  hipError_t e = launch_sort(len, R, nB, row_ptr, order, s);
+  if (e != hipSuccess) return e;
   CARNATOR_ROWS(fill_kernel, mask, R, nB, row_ptr, col_idx);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack(const uint8_t *mask, int64_t R, int nB, uint64_t *bits, hipStream_t s) {
+  if (R == 0) return hipSuccess;
+  const unsigned g = (unsigned)((R + 3) / 4);
+  const int nc = (nB + 63) / 64;
+  CARNATOR_ROWS(pack_kernel, mask, R, nB, bits);
+  return hipGetLastError();
+}
 #undef CARNATOR_ROWS
+
+hipError_t launch_unpack(const uint64_t *bits, int64_t R, int nB, uint8_t *mask, hipStream_t s) {
+  hipLaunchKernelGGL(unpack_kernel, dim3((unsigned)((R + 3) / 4)), dim3(256), 0, s, bits, R, nB,
+                     mask);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_ones_bits(uint64_t *bits, int64_t R, int nB, hipStream_t s) {
+  const int64_t words = R * ((nB + 63) / 64);
+  hipLaunchKernelGGL(fill_ones_bits_kernel, dim3((unsigned)((words + 255) / 256)), dim3(256), 0, s,
+                     bits, words, nB);
+  return hipGetLastError();
+}
+
+size_t compact_bits_scratch_bytes(int64_t R, int B, int nB) {
+  return compact_scratch_bytes(R) + align_up((size_t)B * ((nB + 63) / 64) * sizeof(uint64_t));
+}
+
+hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const uint8_t *rows,
+                               const uint8_t *cols, int32_t *row_ptr, int32_t *col_idx,
+                               int32_t *order, void *scratch, hipStream_t s) {
+  const int64_t R = (int64_t)B * H * nB;
+  int32_t *len = static_cast<int32_t *>(scratch);
+  uint64_t *colw = nullptr;
+  hipError_t e;
+  if (cols != nullptr) {
+    // the dense-column flags of each batch entry, packed once like a mask row
+    colw = reinterpret_cast<uint64_t *>(static_cast<char *>(scratch) + compact_scratch_bytes(R));
+    if ((e = launch_pack(cols, B, nB, colw, s)) != hipSuccess) return e;
+  }
+  const int nw = (nB + 63) / 64;  // nB <= 2048
+  const int HnB = H * nB;
+  int G = 1;
+  while (G < nw) G <<= 1;
+  const unsigned gc = (unsigned)((R + 4 * (64 / G) - 1) / (4 * (64 / G)));
+  switch (G) {
+#define CARNATOR_G(GG)                                                                            \
+  case GG:                                                                                        \
+    hipLaunchKernelGGL(count_bits_kernel<GG>, dim3(gc), dim3(256), 0, s, bits, (int)R, nB, HnB,   \
+                       rows, colw, len);                                                          \
+    break;
+    CARNATOR_G(1) CARNATOR_G(2) CARNATOR_G(4) CARNATOR_G(8) CARNATOR_G(16) CARNATOR_G(32)
+#undef CARNATOR_G
+    default: return hipErrorInvalidValue;
+  }
+  if ((e = launch_sort(len, R, nB, row_ptr, order, s)) != hipSuccess) return e;
+  hipLaunchKernelGGL(fill_bits_kernel, dim3((unsigned)((R + 3) / 4)), dim3(256), 0, s, bits,
+                     (int)R, nB, HnB, rows, colw, row_ptr, col_idx);
   return hipGetLastError();
 }
 

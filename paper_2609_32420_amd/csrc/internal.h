@@ -87,9 +87,10 @@ __device__ inline uint64_t wave_max_u64(uint64_t x) {
 hipError_t launch_pool(View q, View k, int B, int H, int N, int d, int bs, double *qbar,
                        double *kbar, hipStream_t s);
 // Scores, softmax over key blocks, top-mass selection with the tie rule; writes
-// uint8 [BH][nB][nB].
+// uint8 [BH][nB][nB] to mask, or, when bits is non-NULL (mask then unused),
+// bit-packed uint64 [BH][nB][ceil(nB / 64)].
 hipError_t launch_select(const double *qbar, const double *kbar, int BH, int nB, int d,
-                         double sigma, double tau, uint8_t *mask, hipStream_t s);
+                         double sigma, double tau, uint8_t *mask, uint64_t *bits, hipStream_t s);
 hipError_t launch_fill_ones(uint8_t *p, size_t n, hipStream_t s);
 
 // ---- merge -----------------------------------------------------------------
@@ -101,6 +102,19 @@ hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows
 size_t compact_scratch_bytes(int64_t R);
 hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_ptr,
                           int32_t *col_idx, int32_t *order, void *scratch, hipStream_t s);
+
+// ---- bit-packed masks --------------------------------------------------------
+// R rows of nB keep flags as uint64 [R][ceil(nB / 64)], key block j at bit
+// j mod 64 of word j / 64, bits past nB zero.
+hipError_t launch_pack(const uint8_t *mask, int64_t R, int nB, uint64_t *bits, hipStream_t s);
+hipError_t launch_unpack(const uint64_t *bits, int64_t R, int nB, uint8_t *mask, hipStream_t s);
+hipError_t launch_fill_ones_bits(uint64_t *bits, int64_t R, int nB, hipStream_t s);
+// Compaction of the packed mask [B][H][nB] rows widened by rows / cols
+// (uint8 [B][nB] each, or NULL); scratch of compact_bits_scratch_bytes.
+size_t compact_bits_scratch_bytes(int64_t R, int B, int nB);
+hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const uint8_t *rows,
+                               const uint8_t *cols, int32_t *row_ptr, int32_t *col_idx,
+                               int32_t *order, void *scratch, hipStream_t s);
 
 // ---- attention -------------------------------------------------------------
 hipError_t launch_bsattn(View q, View k, View v, uint16_t *out, int64_t osb, int64_t osh,

@@ -116,7 +116,8 @@ template <int D, int E, int R, int W>
 __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict__ qbar,
                                                         const double *__restrict__ kbar, int nB,
                                                         double sigma, double tau,
-                                                        uint8_t *__restrict__ mask, int BH) {
+                                                        uint8_t *__restrict__ mask,
+                                                        uint64_t *__restrict__ bits, int BH) {
   // LDS: [R][nB] logits, then the R pooled query rows, QS doubles apart (a
   // 16-byte pad spreads the 16 rows read by one MFMA step over the banks)
   constexpr int QS = D + 2;
@@ -205,7 +206,7 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
   // and one wave sum.
   for (int r = wave; r < nr; r += W) {
     const double *row = sc + r * nB;
-    uint8_t *out = mask + ((int64_t)bh * nB + r0 + r) * nB;
+    const int64_t grow = (int64_t)bh * nB + r0 + r;
     double pl[E];
     uint64_t key[E];
     double smax = -INFINITY, smin = INFINITY;
@@ -294,8 +295,8 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
         // the one key in [lo, hi), read from the lane that holds it
 #pragma unroll
         for (int u = 0; u < E; ++u) {
-          const unsigned long long bits = __ballot(key[u] >= lo && key[u] < hi);
-          if (bits) kstar = read_lane(key[u], __ffsll((long long)bits) - 1);
+          const unsigned long long hit = __ballot(key[u] >= lo && key[u] < hi);
+          if (hit) kstar = read_lane(key[u], __ffsll((long long)hit) - 1);
         }
         k = cnt_lo;
       } else {
@@ -318,8 +319,10 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
 #pragma unroll
     for (int u = 0; u < E; ++u) nplus += __popcll(__ballot(u * 64 + lane < nB && row[min(u * 64 + lane, nB - 1)] > hiT));
     const int need = k - nplus;
-    // write the row in index order; the first `need` tied blocks are kept
+    // write the row in index order; the first `need` tied blocks are kept.
+    // As bits, the ballot of chunk u is word u of the row, stored by lane u.
     int tied_before = 0;
+    uint64_t word = 0;
 #pragma unroll
     for (int u = 0; u < E; ++u) {
       const int jj = u * 64 + lane;
@@ -329,9 +332,17 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
       const bool tie = ok && fabs(sv - cut) <= kTieEps;
       const unsigned long long tb = __ballot(tie);
       const int rank = tied_before + __popcll(tb & ((1ull << lane) - 1ull));
-      if (ok) out[jj] = (above || (tie && rank < need)) ? 1 : 0;
+      const bool keep = above || (tie && rank < need);
+      if (bits == nullptr) {
+        if (ok) mask[grow * nB + jj] = keep ? 1 : 0;
+      } else {
+        const uint64_t kw = __ballot(keep);
+        word = lane == u ? kw : word;
+      }
       tied_before += __popcll(tb);
     }
+    const int nw = (nB + 63) / 64;
+    if (bits != nullptr && lane < nw) bits[grow * nw + lane] = word;
   }
 }
 
@@ -355,7 +366,8 @@ hipError_t launch_pool(View q, View k, int B, int H, int N, int d, int bs, doubl
 
 template <int D, int R, int W>
 static hipError_t launch_select_dr(const double *qbar, const double *kbar, int BH, int nB,
-                                   double sigma, double tau, uint8_t *mask, hipStream_t s) {
+                                   double sigma, double tau, uint8_t *mask, uint64_t *bits,
+                                   hipStream_t s) {
   const int G = (nB + R - 1) / R * BH;
   dim3 grid((G + 7) / 8 * 8);
   const size_t lds = (size_t)R * (nB + D + 2) * sizeof(double);
@@ -366,7 +378,7 @@ static hipError_t launch_select_dr(const double *qbar, const double *kbar, int B
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);     \
     if (e != hipSuccess) return e;                                                                \
     hipLaunchKernelGGL((select_kernel<D, EE, R, W>), grid, dim3(64 * W), lds, s, qbar, kbar, nB, \
-                       sigma, tau, mask, BH);                                                     \
+                       sigma, tau, mask, bits, BH);                                               \
   } while (0)
   // W = 16 waves (1024 threads, at most 128 VGPRs) only while a lane holds at
   // most 8 positions; the launcher picks R and W accordingly
@@ -402,16 +414,18 @@ static hipError_t launch_select_dr(const double *qbar, const double *kbar, int B
 // workgroup, else W = 8 (two rows each when R = 16).
 template <int D>
 static hipError_t launch_select_d(const double *qbar, const double *kbar, int BH, int nB,
-                                  double sigma, double tau, uint8_t *mask, hipStream_t s) {
-  if (nB <= 512) return launch_select_dr<D, 16, 16>(qbar, kbar, BH, nB, sigma, tau, mask, s);
-  if (nB <= 1024) return launch_select_dr<D, 16, 8>(qbar, kbar, BH, nB, sigma, tau, mask, s);
-  return launch_select_dr<D, 8, 8>(qbar, kbar, BH, nB, sigma, tau, mask, s);
+                                  double sigma, double tau, uint8_t *mask, uint64_t *bits,
+                                  hipStream_t s) {
+  if (nB <= 512) return launch_select_dr<D, 16, 16>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
+  if (nB <= 1024) return launch_select_dr<D, 16, 8>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
+  return launch_select_dr<D, 8, 8>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
 }
 
 hipError_t launch_select(const double *qbar, const double *kbar, int BH, int nB, int d,
-                         double sigma, double tau, uint8_t *mask, hipStream_t s) {
-  if (d == 128) return launch_select_d<128>(qbar, kbar, BH, nB, sigma, tau, mask, s);
-  return launch_select_d<64>(qbar, kbar, BH, nB, sigma, tau, mask, s);
+                         double sigma, double tau, uint8_t *mask, uint64_t *bits,
+                         hipStream_t s) {
+  if (d == 128) return launch_select_d<128>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
+  return launch_select_d<64>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
 }
 
 hipError_t launch_fill_ones(uint8_t *p, size_t n, hipStream_t s) {

@@ -41,7 +41,9 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert L.carnator_abi_version() == 1
+    assert L.carnator_abi_version() == P.ABI_VERSION
+    declared = re.search(r"#define CARNATOR_ABI_VERSION (\d+)", open(HEADER).read())
+    assert int(declared.group(1)) == P.ABI_VERSION
     assert L.carnator_status_str(0) == b"ok"
     for code in (-1, -2, -3, -4, -5, -6):
         assert L.carnator_status_str(code) not in (b"", b"unknown status")
@@ -166,3 +168,43 @@ def test_python_binding_raises_without_gpu_tensors():
     x = torch.zeros(1, 1, 64, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         P.block_sparse_attn(x, x, x, torch.ones(1, 1, 1, 1, dtype=torch.uint8), 64)
+
+
+def test_bit_packed_entry_points_reject(L):
+    s = _shape()
+    p = ctypes.c_void_p(0x1000)
+    odd = ctypes.c_void_p(0x1004)
+    # pack / unpack
+    assert L.carnator_pack_block_mask(None, ctypes.byref(s), p, None) == -1
+    assert L.carnator_pack_block_mask(p, ctypes.byref(s), None, None) == -1
+    assert L.carnator_pack_block_mask(p, ctypes.byref(s), odd, None) == -4
+    assert L.carnator_pack_block_mask(p, ctypes.byref(_shape(bs=32)), p, None) == -3
+    assert L.carnator_unpack_block_mask(None, ctypes.byref(s), p, None) == -1
+    assert L.carnator_unpack_block_mask(odd, ctypes.byref(s), p, None) == -4
+    assert L.carnator_unpack_block_mask(p, None, p, None) == -1
+    # compaction from bits
+    c = L.carnator_compact_block_mask_bits
+    assert c(None, ctypes.byref(s), None, None, p, p, p, p, 1 << 20, None) == -1
+    assert c(p, ctypes.byref(s), None, None, p, None, p, p, 1 << 20, None) == -1
+    assert c(odd, ctypes.byref(s), None, None, p, p, p, p, 1 << 20, None) == -4
+    assert c(p, ctypes.byref(s), None, None, p, p, p, p, 4, None) == -5
+    assert c(p, ctypes.byref(s), None, None, p, p, p, None, 1 << 20, None) == -5
+    assert c(p, ctypes.byref(s), None, None, p, p, p, ctypes.c_void_p(0x1010), 1 << 20, None) == -4
+    # builder to bits: the same checks as the uint8 builder, plus bits alignment
+    q = _view()
+    b = lambda out, tau=0.9, n=1 << 30: L.carnator_build_block_mask_bits(
+        ctypes.byref(q), ctypes.byref(q), ctypes.byref(s), 0.0, tau, out, ctypes.c_void_p(0x40000), n, None)
+    assert b(None) == -1
+    assert b(odd) == -4
+    assert b(p, tau=0.0) == -2
+    assert b(p, n=16) == -5
+    assert "workspace" in _err(L)
+
+
+def test_bit_packed_workspace_size(L):
+    s = _shape(1, 12, 32760, 128, 128)
+    R = 12 * 256
+    # the list lengths, then the packed dense-column words of each batch entry
+    assert L.carnator_compact_block_mask_bits_workspace_size(ctypes.byref(s)) == 12288 + 256
+    assert L.carnator_compact_block_mask_bits_workspace_size(ctypes.byref(_shape(d=96))) == 0
+    assert R * 4 == 12288

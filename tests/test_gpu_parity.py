@@ -174,6 +174,102 @@ def test_compaction_bit_exact(nb, density, heads):
     np.testing.assert_array_equal(order.cpu().numpy(), word)
 
 
+# ---------------------------------------------------------------- bit-packed masks
+
+def _u64(bits: torch.Tensor) -> np.ndarray:
+    return bits.cpu().numpy().view(np.uint64)
+
+
+@pytest.mark.parametrize("nb,heads", [(1, 3), (3, 5), (64, 2), (139, 5), (256, 4), (931, 2), (2048, 1)])
+def test_pack_unpack_bit_exact(nb, heads):
+    m = synth.random_mask(2, heads, nb, 0.3, nb) * np.uint8(3)  # nonzero bytes other than 1
+    bits = P.pack_block_mask(torch.as_tensor(m, device=DEV))
+    np.testing.assert_array_equal(_u64(bits), oracle.pack_mask(m))
+    # unpack from words whose unused high bits are set: they are ignored
+    dirty = oracle.pack_mask(m)
+    if nb % 64:
+        dirty[..., -1] |= ~((np.uint64(1) << np.uint64(nb % 64)) - np.uint64(1))
+    got = P.unpack_block_mask(torch.as_tensor(dirty.view(np.int64), device=DEV))
+    np.testing.assert_array_equal(got.cpu().numpy(), oracle.unpack_mask(dirty, nb))
+
+
+@pytest.mark.parametrize("wid", [0, 1, 2, 4])
+def test_mask_builder_bits_bit_exact(wid):
+    wl, x = _inputs(wid, heads=2 if wid else None)
+    want, fragile = _oracle_mask(x, wl)
+    bits = P.build_block_mask_bits(x["q_hist"], x["k_hist"], wl.block, wl.tau)
+    got = oracle.unpack_mask(_u64(bits), wl.n_blocks)
+    _assert_masks_equal(torch.as_tensor(got), want, fragile, wl.tau)
+    # unused high bits of each row's last word are written as 0
+    if wl.n_blocks % 64:
+        assert not (_u64(bits)[..., -1] >> np.uint64(wl.n_blocks % 64)).any()
+
+
+@pytest.mark.parametrize("nb", [3, 100, 256])
+def test_mask_builder_bits_full_threshold(nb):
+    x = torch.randn(1, 2, nb * 64 - 5, 64, device=DEV).to(torch.bfloat16)
+    bits = P.build_block_mask_bits(x, x, 64, 1.0)
+    np.testing.assert_array_equal(_u64(bits), oracle.pack_mask(np.ones((1, 2, nb, nb), dtype=np.uint8)))
+
+
+# widened or not; R = heads * nb rows (2048 x 7 reads the lengths from memory
+# in the sort, as for the uint8 compaction)
+@pytest.mark.parametrize("nb,density,heads,widen", [(3, 0.5, 5, False), (139, 0.3, 5, True), (256, 0.2, 5, True),
+                                                    (256, 0.2, 5, False), (931, 0.1, 3, True),
+                                                    (2048, 0.05, 7, True), (64, 1.0, 3, False)])
+def test_compaction_from_bits_bit_exact(nb, density, heads, widen):
+    B = 2
+    m = synth.random_mask(B, heads, nb, density, nb + 7)
+    m[0, 1, 0] = 0
+    rows = cols = None
+    if widen:
+        rng = np.random.default_rng(nb)
+        rows = (rng.random((B, nb)) < 0.1).astype(np.uint8)
+        cols = (rng.random((B, nb)) < 0.05).astype(np.uint8) * np.uint8(9)
+    bits = oracle.pack_mask(m)
+    if nb % 64:
+        bits[..., -1] |= np.uint64(1) << np.uint64(63)  # an unused bit set: ignored
+    dbits = torch.as_tensor(bits.view(np.int64), device=DEV)
+    before = dbits.clone()
+    rp, ci, order = P.compact_block_mask_bits(dbits, rows, cols)
+    merged = oracle.merge_target_rows(m, rows, cols) if widen else m
+    wrp, wci, word = oracle.compact_mask(merged)
+    np.testing.assert_array_equal(rp.cpu().numpy(), wrp)
+    np.testing.assert_array_equal(ci.cpu().numpy(), wci)
+    np.testing.assert_array_equal(order.cpu().numpy(), word)
+    assert torch.equal(dbits, before)  # the stored mask is only read
+
+
+def test_mask_bank_record_and_reuse():
+    # a bank of 2 steps x 2 branches x 2 layers for the tiny workload: each
+    # slot recorded from its own historical Q/K, then compacted for the target
+    # and walked by the attention kernel
+    wl = synth.WORKLOADS[0]
+    bank = P.MaskBank(2, 2, 2, 1, 2, wl.n_blocks, device=DEV)
+    assert bank.nbytes == 8 * 2 * 2 * 2 * 2 * wl.n_blocks * 1
+    want = {}
+    for t in range(2):
+        for c in range(2):
+            for layer in range(2):
+                seed = 100 * t + 10 * c + layer
+                x = synth.attention_inputs(wl, seed=seed, device=DEV)
+                bank.record(t, c, layer, x["q_hist"], x["k_hist"], wl.block, wl.tau)
+                want[(t, c, layer)] = (x, _oracle_mask(x, wl))
+    for (t, c, layer), (x, (m, fragile)) in want.items():
+        _say("slot", t, c, layer)
+        got = oracle.unpack_mask(_u64(bank.slot(t, c, layer)), wl.n_blocks)
+        _assert_masks_equal(torch.as_tensor(got), m, fragile, wl.tau)
+        lists = bank.lists(t, c, layer, x["row_flags"])
+        merged = oracle.merge_target_rows(got, x["row_flags"].cpu().numpy())
+        for g, w in zip(lists, oracle.compact_mask(merged)):
+            np.testing.assert_array_equal(g.cpu().numpy(), w)
+        o = P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists, wl.block)
+        o_ref, _ = oracle.block_sparse_attention(oracle.to_f64(x["q"]), oracle.to_f64(x["k"]),
+                                                 oracle.to_f64(x["v"]), merged, wl.block)
+        rows = [(0, h, i) for h in range(2) for i in range(wl.n_blocks)]
+        _compare_rows(o, o_ref, None, None, rows, wl.seq_len, wl.block)
+
+
 # ---------------------------------------------------------------- attention
 
 def test_attention_tiny_workload_full():

@@ -205,3 +205,66 @@ def test_compact_roundtrip_and_order():
     assert sorted(order.tolist()) == list(range(R))
     for a, b in zip(order[:-1], order[1:]):
         assert lens[a] > lens[b] or (lens[a] == lens[b] and a < b)
+
+
+# ---------------------------------------------------------------- bit-packed masks
+
+def test_pack_single_bits_by_hand():
+    # every column of a 130-wide row alone: exactly bit j mod 64 of word j // 64
+    nb = 130
+    for j in range(nb):
+        m = np.zeros((1, nb), dtype=np.uint8)
+        m[0, j] = 7
+        w = oracle.pack_mask(m)
+        assert w.shape == (1, 3) and w.dtype == np.uint64
+        want = [0, 0, 0]
+        want[j // 64] = 1 << (j % 64)
+        assert [int(x) for x in w[0]] == want, j
+
+
+@pytest.mark.parametrize("nb", [1, 3, 63, 64, 65, 139, 256, 931])
+def test_pack_matches_numpy_packbits(nb):
+    # little-endian bit order within bytes and words: packbits(bitorder="little")
+    # laid out as little-endian uint64 is the same encoding
+    rng = np.random.default_rng(nb)
+    m = (rng.random((2, 3, nb, nb)) < 0.3).astype(np.uint8) * rng.integers(1, 255, (2, 3, nb, nb)).astype(np.uint8)
+    w = (nb + 63) // 64
+    pb = np.packbits(m != 0, axis=-1, bitorder="little")
+    padded = np.zeros(m.shape[:-1] + (w * 8,), dtype=np.uint8)
+    padded[..., :pb.shape[-1]] = pb
+    np.testing.assert_array_equal(oracle.pack_mask(m), padded.view("<u8"))
+
+
+@pytest.mark.parametrize("nb", [1, 64, 100, 200])
+def test_unpack_inverts_pack_and_ignores_padding(nb):
+    rng = np.random.default_rng(nb + 1)
+    m = (rng.random((4, nb, nb)) < 0.5).astype(np.uint8)
+    bits = oracle.pack_mask(m)
+    np.testing.assert_array_equal(oracle.unpack_mask(bits, nb), m)
+    if nb % 64:
+        # the high bits of the last word are 0 when packed and ignored when read
+        assert not (bits[..., -1] >> np.uint64(nb % 64)).any()
+        dirty = bits.copy()
+        dirty[..., -1] |= ~((np.uint64(1) << np.uint64(nb % 64)) - np.uint64(1))
+        np.testing.assert_array_equal(oracle.unpack_mask(dirty, nb), m)
+    # popcount of a row's words = its number of kept blocks
+    pc = np.array([[bin(int(x)).count("1") for x in row] for row in bits.reshape(-1, bits.shape[-1])])
+    np.testing.assert_array_equal(pc.sum(axis=1), m.reshape(-1, nb).sum(axis=1))
+
+
+def test_pack_full_and_empty_rows():
+    for nb, last in ((64, 2**64 - 1), (70, 2**6 - 1), (128, 2**64 - 1), (1, 1)):
+        full = oracle.pack_mask(np.ones((nb, nb), dtype=np.uint8))
+        assert all(int(x) == 2**64 - 1 for x in full[:, :-1].ravel())
+        assert all(int(x) == last for x in full[:, -1])
+        assert not oracle.pack_mask(np.zeros((nb, nb), dtype=np.uint8)).any()
+
+
+def test_bank_slot_size():
+    # one stored mask per (step, branch, layer): a 256-block Wan-shaped mask of
+    # 12 heads takes 12 * 256 * 4 words; 50 steps x 2 branches x 30 layers of
+    # them are 294,912,000 bytes, an eighth of the uint8 masks
+    bits = oracle.pack_mask(np.zeros((1, 12, 256, 256), dtype=np.uint8))
+    assert bits.shape == (1, 12, 256, 4)
+    assert bits.nbytes * 50 * 2 * 30 == 294_912_000
+    assert bits.nbytes * 8 == 12 * 256 * 256
