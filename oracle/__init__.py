@@ -20,6 +20,11 @@ Every function is plain fp64 NumPy, written from the paper's definitions:
   executor walks.
 * ``pack_mask`` / ``unpack_mask``: the masks as one bit per block pair, the
   form in which they are stored per step, branch and layer (Appendix C.3).
+* ``dilate_frames`` / ``chebyshev_distance`` / ``regions`` / ``smoothstep`` /
+  ``latent_fusion`` / ``region_block_flags`` / ``restrict_mask`` /
+  ``compact_restricted``: the region-restricted middle-layer path (Sec. 3.3
+  "Region-Guided Latent Reuse" and "Joint Reuse in Intermediate Layers";
+  Appendix C.3 radii).
 * ``block_sparse_attention``: softmax attention of the recomputed target
   Q, K, V restricted to the reused block structure (Sec. 3.3, "Historical
   Sparse-Connectivity Reuse"; Appendix C.3).
@@ -34,6 +39,8 @@ from .mask import (pool_blocks, block_scores, select_row, build_block_mask,
                    merge_target_rows, compact_mask, row_admissible_masks, TIE_EPS,
                    FRAGILE_EPS, pack_mask, unpack_mask)
 from .attention import block_sparse_attention, token_mask_from_blocks
+from .region import (dilate_frames, chebyshev_distance, smoothstep, regions, latent_fusion,
+                     region_block_flags, restrict_mask, compact_restricted)
 from .cosine import cosine_similarity, topk_cosine
 from .convert import to_f64
 
@@ -42,4 +49,6 @@ __all__ = [
     "merge_target_rows", "compact_mask", "row_admissible_masks", "TIE_EPS",
     "FRAGILE_EPS", "pack_mask", "unpack_mask", "block_sparse_attention", "token_mask_from_blocks",
     "cosine_similarity", "topk_cosine", "to_f64",
+    "dilate_frames", "chebyshev_distance", "smoothstep", "regions", "latent_fusion",
+    "region_block_flags", "restrict_mask", "compact_restricted",
 ]

@@ -96,7 +96,7 @@ WORKLOADS = {
 SIG_M, SIG_D, SIG_TOPK, SIG_NQ = WORKLOADS[2].sig
 
 _STREAMS = ("qk_field", "v_field", "q_noise", "k_noise", "v_noise",
-            "qh_noise", "kh_noise", "text", "region", "signature")
+            "qh_noise", "kh_noise", "text", "region", "signature", "evidence", "latent")
 
 
 def _children(seed: int, wid: int) -> dict:
@@ -282,3 +282,47 @@ def random_mask(batch: int, heads: int, nb: int, density: float, seed: int = 0) 
     """Uniform random 0/1 block mask (for boundary and edge-case tests)."""
     rng = np.random.default_rng(np.random.SeedSequence([seed, 99]))
     return (rng.random((batch, heads, nb, nb)) < density).astype(np.uint8)
+
+
+def evidence_region(wl: Workload, seed: int = 0) -> np.ndarray:
+    """An object-like evidence region on the token grid, uint8 [B, T, H, W].
+
+    Per frame, the tokens inside an ellipse whose centre drifts linearly over
+    the frames, with radii of 1/6 to 1/4 of the frame, and a ragged boundary
+    (tokens within one token of the ellipse edge flipped with probability
+    0.3).  A random quarter of the frames (never all) hold no evidence.
+    """
+    kids = _children(seed, wl.wid)
+    rng = np.random.default_rng(kids["evidence"])
+    T, H, W = wl.grid
+    out = np.zeros((wl.batch, T, H, W), dtype=np.uint8)
+    yy, xx = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    for b in range(wl.batch):
+        c0 = np.array([rng.uniform(0.25, 0.75) * H, rng.uniform(0.25, 0.75) * W])
+        drift = rng.uniform(-0.15, 0.15, size=2) * np.array([H, W]) / max(T, 1)
+        radii = np.array([rng.uniform(1 / 6, 1 / 4) * H, rng.uniform(1 / 6, 1 / 4) * W])
+        empty = rng.random(T) < 0.25
+        if empty.all():
+            empty[rng.integers(0, T)] = False
+        for t in range(T):
+            if empty[t]:
+                continue
+            cy, cx = c0 + drift * t
+            r = np.sqrt(((yy - cy) / radii[0]) ** 2 + ((xx - cx) / radii[1]) ** 2)
+            inside = r <= 1.0
+            edge = np.abs(r - 1.0) * min(radii) <= 1.0
+            flip = edge & (rng.random((H, W)) < 0.3)
+            out[b, t] = (inside ^ flip).astype(np.uint8)
+    return out
+
+
+def latents(wl: Workload, channels: int = 16, patch=(1, 2, 2), seed: int = 0, device="cpu"):
+    """Target-updated and historical latents, fp32 [B, C, T*pt, H*ph, W*pw]
+    of N(0, 1) (the scale of a diffusion latent)."""
+    kids = _children(seed, wl.wid)
+    T, H, W = wl.grid
+    shape = (wl.batch, channels, T * patch[0], H * patch[1], W * patch[2])
+    g = _torch_gen(kids["latent"], "cpu")
+    zt = torch.randn(shape, generator=g, dtype=torch.float32)
+    zh = torch.randn(shape, generator=g, dtype=torch.float32)
+    return zt.to(device), zh.to(device)

@@ -59,3 +59,17 @@ def test_historical_density_in_band():
     x = synth.attention_inputs(wl, seed=0)
     m, rep = oracle.build_block_mask(oracle.to_f64(x["q_hist"]), oracle.to_f64(x["k_hist"]), wl.block, wl.tau)
     assert 0.15 <= m.mean() <= 0.25
+
+
+def test_evidence_region_is_seeded_and_object_like():
+    import oracle
+    for wid in (0, 1, 3):
+        wl = synth.WORKLOADS[wid]
+        a = synth.evidence_region(wl, seed=2)
+        b = synth.evidence_region(wl, seed=2)
+        np.testing.assert_array_equal(a, b)
+        assert a.shape == (wl.batch,) + tuple(wl.grid)
+        assert 0.0 < a.mean() < 0.3
+        assert not (synth.evidence_region(wl, seed=3) == a).all()
+    code, _ = oracle.regions(synth.evidence_region(synth.WORKLOADS[1]))
+    assert all((code == k).any() for k in range(4))
