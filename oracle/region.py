@@ -141,7 +141,7 @@ def compact_restricted(mask: np.ndarray, active_q: np.ndarray, context_k: np.nda
     m = restrict_mask(mask, active_q, context_k)
     B, H, nb, _ = m.shape
     flat = m.reshape(-1, nb)
-    counts = flat.sum(axis=1)
+    counts = flat.sum(axis=1, dtype=np.int64)  # signed: the order negates it
     row_ptr = np.zeros(flat.shape[0] + 1, dtype=np.int64)
     row_ptr[1:] = np.cumsum(counts)
     col_idx = np.nonzero(flat)[1]

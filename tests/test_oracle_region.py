@@ -159,3 +159,25 @@ def test_restricted_order_puts_active_rows_first():
     assert (lens[od[n:]] == 0).all()
     # no list holds a non-context key block
     assert not np.isin(ci, [2]).any()
+
+
+def test_restricted_order_brute_force_with_empty_active_rows():
+    # active rows of every length, including empty ones, sorted by
+    # (-length, row) with plain Python; the inactive rows follow in row order
+    rng = np.random.default_rng(12)
+    m = (rng.random((2, 3, 7, 7)) < 0.4).astype(np.uint8)
+    m[0, 1, 2] = 0  # an active row with nothing kept
+    act = np.array([[1, 0, 1, 1, 0, 1, 0], [0, 1, 1, 0, 1, 0, 1]], np.uint8)
+    ctx = np.array([[1, 1, 0, 1, 1, 1, 1], [1, 1, 1, 0, 1, 1, 0]], np.uint8)
+    rp, ci, od, n = oracle.compact_restricted(m, act, ctx)
+    lens = {}
+    for b in range(2):
+        for h in range(3):
+            for i in range(7):
+                r = (b * 3 + h) * 7 + i
+                lens[r] = sum(1 for j in range(7) if m[b, h, i, j] and act[b, i] and ctx[b, j])
+    active = [r for r in range(42) if act[r // 21, r % 7]]
+    want = sorted(active, key=lambda r: (-lens[r], r)) + [r for r in range(42) if r not in active]
+    assert list(od) == want and n == len(active)
+    assert lens[(0 * 3 + 1) * 7 + 2] == 0 and any(lens[r] > 0 for r in active)
+    np.testing.assert_array_equal(np.diff(rp), [lens[r] for r in range(42)])
