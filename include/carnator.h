@@ -17,6 +17,13 @@
  *   carnator_block_sparse_attn  attention of the recomputed target Q, K, V
  *                               under the reused structure (Sec. 3.3,
  *                               historical sparse-connectivity reuse)
+ *   carnator_region_weights, carnator_latent_fusion,
+ *   carnator_region_block_flags, carnator_compact_block_mask_bits_region,
+ *   carnator_block_sparse_attn_rows
+ *                               region-restricted reuse in the middle layers
+ *                               (Sec. 3.3, region-guided latent reuse and
+ *                               joint reuse in intermediate layers; Appendix
+ *                               C.3)
  *   carnator_signature_sim      cosine scoring of an early-step signature
  *                               against a bank of cached signatures (Sec. 3.1,
  *                               Sec. 4.1 candidate recall)
@@ -67,7 +74,7 @@
 extern "C" {
 #endif
 
-#define CARNATOR_ABI_VERSION 2
+#define CARNATOR_ABI_VERSION 3
 
 typedef enum {
   CARNATOR_OK = 0,
@@ -213,6 +220,97 @@ int carnator_compact_block_mask_bits(const uint64_t *bits, const carnator_shape 
                                      const uint8_t *target_rows, const uint8_t *dense_cols,
                                      int32_t *row_ptr, int32_t *col_idx, int32_t *order,
                                      void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Region-restricted reuse in the middle layers.
+ *
+ * Sec. 3.3 ("Region-Guided Latent Reuse"): the Evidence Region of the
+ * accepted cache is expanded into an Active Region and a larger Context
+ * Region (evidence within active within context) on the T x H x W token
+ * grid; each later latent is z = W * z_target + (1 - W) * z_hist with
+ * W = 1 on the evidence, W = 1 - s(d / d_max) on the transition band (active
+ * minus evidence) and W = 0 outside the active region, s the smoothstep
+ * 3 t^2 - 2 t^3, d the Chebyshev distance to the evidence within the token's
+ * frame and d_max its largest value over the band of the batch entry.
+ * Appendix C.3: active = evidence dilated by 2 tokens, context = active
+ * dilated by 3 more, per latent frame on the H x W grid (dilation by the
+ * (2r+1) x (2r+1) square).  Sec. 3.3 ("Joint Reuse in Intermediate Layers"):
+ * in the middle layers only the historical connectivity of active queries to
+ * context keys is kept; tokens outside the active region keep their cached
+ * computation.
+ *
+ * carnator_region_weights: region codes and W from the evidence.
+ *   evidence   uint8 [B, T, H, W], nonzero = evidence token
+ *   r_active, r_context  dilation radii (2 and 3 in the paper);
+ *              r_active + r_context <= 250
+ *   region     uint8 [B, T, H, W] out: 3 evidence, 2 band, 1 context minus
+ *              active, 0 outside the context region
+ *   weight     fp32 [B, T, H, W] out: W
+ *   workspace  carnator_region_weights_workspace_size(B, T, H, W) bytes,
+ *              256-byte aligned
+ *   H * W <= 65536 tokens per frame (else E_UNSUPPORTED).
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_WORKSPACE, E_HIP.
+ *
+ * carnator_latent_fusion: z_out = W * z_target + (1 - W) * z_hist.
+ *   z_target, z_hist, z_out  fp32 [B, C, T, H, W] contiguous (latent grid);
+ *              z_out may be z_target or z_hist
+ *   weight     fp32 [B, T / patch_t, H / patch_h, W / patch_w] (token grid);
+ *              a latent element takes the weight of the token whose patch
+ *              holds it (patch sizes >= 1 dividing T, H, W)
+ * Errors: E_NULL, E_SHAPE, E_ALIGN (4-byte), E_HIP.
+ *
+ * carnator_region_block_flags: active query blocks and context key blocks.
+ *   region     uint8 [B, N - n_text]: the codes of the video tokens in the
+ *              attention's (t, y, x) raster order
+ *   n_text     text tokens placed before the video tokens (they carry the
+ *              target prompt and count as active and as context)
+ *   shape      batch, seq_len = N, block (head fields as for any call)
+ *   active_q   uint8 [B, nB] out: 1 if a token of query block i is active
+ *              (code >= 2 or text)
+ *   context_k  uint8 [B, nB] out: 1 if a token of key block j is context
+ *              (code >= 1 or text)
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_HIP.
+ *
+ * carnator_compact_block_mask_bits_region: the lists of the stored mask
+ * restricted to active rows and context columns,
+ * M'[b,h,i,j] = M[b,h,i,j] and active_q[b,i] and context_k[b,j].
+ *   bits, row_ptr, col_idx: as carnator_compact_block_mask_bits
+ *   order      int32 [R]: the active rows by descending list length (lower
+ *              row first on equal length), then the inactive rows in
+ *              ascending order (their lists are empty)
+ *   n_active   int32 [1] out (device): the number of active rows
+ *   workspace  carnator_compact_block_mask_bits_workspace_size(shape) bytes
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_WORKSPACE, E_HIP.
+ *
+ * carnator_block_sparse_attn_rows: carnator_block_sparse_attn_lists over
+ * the rows order[0 .. *n_rows) only (n_rows a device int32, e.g. the
+ * n_active written above); the output and LSE of every other row are left
+ * untouched.  Errors: as carnator_block_sparse_attn_lists.
+ */
+size_t carnator_region_weights_workspace_size(int32_t batch, int32_t frames, int32_t height,
+                                              int32_t width);
+int carnator_region_weights(const uint8_t *evidence, int32_t batch, int32_t frames, int32_t height,
+                            int32_t width, int32_t r_active, int32_t r_context, uint8_t *region,
+                            float *weight, void *workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+int carnator_latent_fusion(const float *z_target, const float *z_hist, const float *weight,
+                           float *z_out, int32_t batch, int32_t channels, int32_t frames,
+                           int32_t height, int32_t width, int32_t patch_t, int32_t patch_h,
+                           int32_t patch_w, hipStream_t stream);
+int carnator_region_block_flags(const uint8_t *region, int32_t n_text, const carnator_shape *shape,
+                                uint8_t *active_q, uint8_t *context_k, hipStream_t stream);
+int carnator_compact_block_mask_bits_region(const uint64_t *bits, const carnator_shape *shape,
+                                            const uint8_t *active_q, const uint8_t *context_k,
+                                            int32_t *row_ptr, int32_t *col_idx, int32_t *order,
+                                            int32_t *n_active, void *workspace,
+                                            size_t workspace_bytes, hipStream_t stream);
+int carnator_block_sparse_attn_rows(const carnator_view *q, const carnator_view *k,
+                                    const carnator_view *v, void *out, int64_t out_stride_b,
+                                    int64_t out_stride_h, int64_t out_stride_n,
+                                    const carnator_shape *shape, const int32_t *row_ptr,
+                                    const int32_t *col_idx, const int32_t *order,
+                                    const int32_t *n_rows, float scale, float *lse,
+                                    hipStream_t stream);
 
 /*
  * Block-sparse attention -- Sec. 3.3 ("Historical Sparse-Connectivity

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libcarnator.so")
 
 CARNATOR_OK = 0
 # CARNATOR_ABI_VERSION of include/carnator.h this binding marshals for
-ABI_VERSION = 2
+ABI_VERSION = 3
 STATUS = {0: "OK", -1: "E_NULL", -2: "E_SHAPE", -3: "E_UNSUPPORTED", -4: "E_ALIGN",
           -5: "E_WORKSPACE", -6: "E_HIP"}
 
@@ -31,6 +31,9 @@ EXPORTS = (
     "carnator_compact_block_mask_workspace_size", "carnator_compact_block_mask",
     "carnator_build_block_mask_bits", "carnator_pack_block_mask", "carnator_unpack_block_mask",
     "carnator_compact_block_mask_bits_workspace_size", "carnator_compact_block_mask_bits",
+    "carnator_region_weights_workspace_size", "carnator_region_weights", "carnator_latent_fusion",
+    "carnator_region_block_flags", "carnator_compact_block_mask_bits_region",
+    "carnator_block_sparse_attn_rows",
     "carnator_block_sparse_attn_workspace_size", "carnator_block_sparse_attn",
     "carnator_block_sparse_attn_lists",
     "carnator_signature_sim_workspace_size", "carnator_signature_sim",
@@ -80,6 +83,13 @@ def lib() -> ctypes.CDLL:
             "carnator_unpack_block_mask": (ctypes.c_int, [P, SP, P, P]),
             "carnator_compact_block_mask_bits_workspace_size": (SZ, [SP]),
             "carnator_compact_block_mask_bits": (ctypes.c_int, [P, SP, P, P, P, P, P, P, SZ, P]),
+            "carnator_region_weights_workspace_size": (SZ, [I32, I32, I32, I32]),
+            "carnator_region_weights": (ctypes.c_int, [P, I32, I32, I32, I32, I32, I32, P, P, P, SZ, P]),
+            "carnator_latent_fusion": (ctypes.c_int, [P, P, P, P, I32, I32, I32, I32, I32, I32, I32, I32, P]),
+            "carnator_region_block_flags": (ctypes.c_int, [P, I32, SP, P, P, P]),
+            "carnator_compact_block_mask_bits_region": (ctypes.c_int, [P, SP, P, P, P, P, P, P, P, SZ, P]),
+            "carnator_block_sparse_attn_rows": (ctypes.c_int, [VP, VP, VP, P, I64, I64, I64, SP, P, P, P, P,
+                                                               F32, P, P]),
             "carnator_block_sparse_attn_workspace_size": (SZ, [SP]),
             "carnator_block_sparse_attn": (ctypes.c_int, [VP, VP, VP, P, I64, I64, I64, SP, P, F32, P, P,
                                                           SZ, P]),
@@ -394,9 +404,13 @@ def block_sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, mask: t
 
 
 def block_sparse_attn_lists(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, lists, block: int,
-                            scale: float = 0.0, return_lse: bool = False, out: Optional[torch.Tensor] = None):
+                            scale: float = 0.0, return_lse: bool = False, out: Optional[torch.Tensor] = None,
+                            n_rows: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None):
     """block_sparse_attn with the mask given as the (row_ptr, col_idx, order)
-    lists of compact_block_mask (carnator_block_sparse_attn_lists)."""
+    lists of compact_block_mask (carnator_block_sparse_attn_lists).  With
+    ``n_rows`` (a device int32 tensor of one element) only the rows
+    order[0 .. n_rows) are computed (carnator_block_sparse_attn_rows); the
+    rest of ``out`` (and of ``lse``, which may be passed in) is untouched."""
     s = _shape(q, block)
     for t, n in ((k, "k"), (v, "v")):
         if tuple(t.shape) != tuple(q.shape):
@@ -411,13 +425,114 @@ def block_sparse_attn_lists(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, l
         raise ValueError("col_idx must be int32 on the GPU")
     if out is None:
         out = torch.empty_like(q, memory_format=torch.contiguous_format)
-    lse = torch.empty(s.batch, s.heads, s.seq_len, dtype=torch.float32, device=q.device) if return_lse else None
+    if return_lse and lse is None:
+        lse = torch.empty(s.batch, s.heads, s.seq_len, dtype=torch.float32, device=q.device)
+    if not return_lse:
+        lse = None
+    elif lse.dtype != torch.float32 or not lse.is_contiguous() or tuple(lse.shape) != (s.batch, s.heads, s.seq_len):
+        raise ValueError("lse must be a contiguous fp32 [B, H, N] tensor")
     qv, kv, vv = _view(q), _view(k), _view(v)
-    _check(lib().carnator_block_sparse_attn_lists(ctypes.byref(qv), ctypes.byref(kv), ctypes.byref(vv), _ptr(out),
-                                                  out.stride(0), out.stride(1), out.stride(2), ctypes.byref(s),
-                                                  _ptr(row_ptr), _ptr(col_idx), _ptr(order), float(scale),
-                                                  _ptr(lse), _stream(q)))
+    if n_rows is None:
+        _check(lib().carnator_block_sparse_attn_lists(ctypes.byref(qv), ctypes.byref(kv), ctypes.byref(vv),
+                                                      _ptr(out), out.stride(0), out.stride(1), out.stride(2),
+                                                      ctypes.byref(s), _ptr(row_ptr), _ptr(col_idx), _ptr(order),
+                                                      float(scale), _ptr(lse), _stream(q)))
+    else:
+        if n_rows.dtype != torch.int32 or not n_rows.is_cuda or n_rows.numel() < 1:
+            raise ValueError("n_rows must be an int32 GPU tensor")
+        _check(lib().carnator_block_sparse_attn_rows(ctypes.byref(qv), ctypes.byref(kv), ctypes.byref(vv),
+                                                     _ptr(out), out.stride(0), out.stride(1), out.stride(2),
+                                                     ctypes.byref(s), _ptr(row_ptr), _ptr(col_idx), _ptr(order),
+                                                     _ptr(n_rows), float(scale), _ptr(lse), _stream(q)))
     return (out, lse) if return_lse else out
+
+
+# ---------------------------------------------------------------- region-restricted reuse
+
+def region_weights(evidence: torch.Tensor, r_active: int = 2, r_context: int = 3, out=None,
+                   workspace: Optional[torch.Tensor] = None):
+    """(region codes uint8, W fp32), both [B, T, H, W], from the evidence
+    uint8 [B, T, H, W] (carnator_region_weights)."""
+    if evidence.dim() != 4 or evidence.dtype != torch.uint8 or not evidence.is_contiguous():
+        raise ValueError("evidence must be a contiguous uint8 [B, T, H, W] tensor")
+    B, T, H, W = evidence.shape
+    dev = evidence.device
+    if out is None:
+        out = (torch.empty(B, T, H, W, dtype=torch.uint8, device=dev),
+               torch.empty(B, T, H, W, dtype=torch.float32, device=dev))
+    region, weight = out
+    if workspace is None:
+        workspace = _workspace(lib().carnator_region_weights_workspace_size(B, T, H, W), dev)
+    _check(lib().carnator_region_weights(_ptr(evidence), B, T, H, W, int(r_active), int(r_context), _ptr(region),
+                                         _ptr(weight), _ptr(workspace), workspace.numel(), _stream(evidence)))
+    return region, weight
+
+
+def latent_fusion(z_target: torch.Tensor, z_hist: torch.Tensor, weight: torch.Tensor, out=None):
+    """W * z_target + (1 - W) * z_hist for fp32 latents [B, C, T, H, W] and W
+    on the token grid [B, T/pt, H/ph, W/pw] (carnator_latent_fusion).  ``out``
+    may be z_target or z_hist."""
+    for t, n in ((z_target, "z_target"), (z_hist, "z_hist")):
+        if t.dim() != 5 or t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous fp32 [B, C, T, H, W] tensor" % n)
+    if tuple(z_hist.shape) != tuple(z_target.shape):
+        raise ValueError("z_hist shape differs from z_target")
+    if weight.dim() != 4 or weight.dtype != torch.float32 or not weight.is_contiguous():
+        raise ValueError("weight must be a contiguous fp32 [B, T, H, W] tensor")
+    B, C, T, H, W = z_target.shape
+    if weight.shape[0] != B or T % weight.shape[1] or H % weight.shape[2] or W % weight.shape[3]:
+        raise ValueError("the weight grid must divide the latent grid")
+    pt, ph, pw = T // weight.shape[1], H // weight.shape[2], W // weight.shape[3]
+    if out is None:
+        out = torch.empty_like(z_target)
+    _check(lib().carnator_latent_fusion(_ptr(z_target), _ptr(z_hist), _ptr(weight), _ptr(out), B, C, T, H, W,
+                                        pt, ph, pw, _stream(z_target)))
+    return out
+
+
+def region_block_flags(region: torch.Tensor, n_text: int, block: int, out=None):
+    """(active query blocks, context key blocks), uint8 [B, nB] each, from the
+    region codes [B, T, H, W] of the video tokens (carnator_region_block_flags)."""
+    if region.dtype != torch.uint8 or not region.is_contiguous():
+        raise ValueError("region must be a contiguous uint8 tensor")
+    B = region.shape[0]
+    N = n_text + region[0].numel()
+    nb = -(-N // block)
+    if out is None:
+        out = (torch.empty(B, nb, dtype=torch.uint8, device=region.device),
+               torch.empty(B, nb, dtype=torch.uint8, device=region.device))
+    s = Shape(B, 1, N, 64, block)
+    _check(lib().carnator_region_block_flags(_ptr(region), int(n_text), ctypes.byref(s), _ptr(out[0]), _ptr(out[1]),
+                                             _stream(region)))
+    return out
+
+
+def compact_block_mask_bits_region(bits: torch.Tensor, active_q, context_k, out=None,
+                                   workspace: Optional[torch.Tensor] = None):
+    """(row_ptr, col_idx, order, n_active) of the packed mask restricted to
+    active rows and context columns (carnator_compact_block_mask_bits_region).
+    col_idx keeps its full capacity and n_active stays on the device (an int32
+    tensor of one element), so nothing synchronises."""
+    B, H, nb = _bits_shape(bits)
+    R = B * H * nb
+    dev = bits.device
+    act = _dev_u8(active_q, dev, (B, nb))
+    ctx = _dev_u8(context_k, dev, (B, nb))
+    s = Shape(B, H, nb * 64, 64, 64)
+    if out is None:
+        out = (torch.empty(R + 1, dtype=torch.int32, device=dev),
+               torch.empty(max(R * nb, 1), dtype=torch.int32, device=dev),
+               torch.empty(R, dtype=torch.int32, device=dev),
+               torch.empty(1, dtype=torch.int32, device=dev))
+    row_ptr, col_idx, order, n_active = out
+    if row_ptr.numel() < R + 1 or col_idx.numel() < R * nb or order.numel() < R or n_active.numel() < 1:
+        raise ValueError("out tensors too small")
+    if workspace is None:
+        workspace = compact_block_mask_bits_workspace(bits)
+    _check(lib().carnator_compact_block_mask_bits_region(_ptr(bits), ctypes.byref(s), _ptr(act), _ptr(ctx),
+                                                         _ptr(row_ptr), _ptr(col_idx), _ptr(order), _ptr(n_active),
+                                                         _ptr(workspace), workspace.numel(), _stream(bits)))
+    return row_ptr, col_idx, order, n_active
 
 
 def signature_sim_workspace(nq: int, m: int, topk: int, device) -> torch.Tensor:

@@ -33,6 +33,10 @@ int hip_fail(hipError_t e, const char *what) {
 }
 
 constexpr int kMaxBlocks = 2048;  // nB limit of the selection kernel
+// region transform: distances are bytes (radius sum < 255) and a frame's
+// evidence and row distances sit in LDS (2 bytes per token)
+constexpr int kMaxRegionRadius = 250;
+constexpr size_t kMaxRegionFrameLds = 128 * 1024;
 
 int check_shape(const carnator_shape *s) {
   if (!s) return fail(CARNATOR_E_NULL, "shape is NULL");
@@ -268,8 +272,98 @@ int carnator_compact_block_mask_bits(const uint64_t *bits, const carnator_shape 
   if ((rc = check_ws(workspace, ws_bytes, carnator_compact_block_mask_bits_workspace_size(s))))
     return rc;
   hipError_t e = launch_compact_bits(bits, s->batch, s->heads, n_blocks(s), target_rows,
-                                     dense_cols, row_ptr, col_idx, order, workspace, stream);
+                                     dense_cols, false, row_ptr, col_idx, order, nullptr, workspace,
+                                     stream);
   if (e != hipSuccess) return hip_fail(e, "compact_bits");
+  return ok();
+}
+
+// ---------------------------------------------------------------- region-restricted reuse
+
+size_t carnator_region_weights_workspace_size(int32_t batch, int32_t frames, int32_t height,
+                                              int32_t width) {
+  if (batch < 1 || frames < 1 || height < 1 || width < 1) return 0;
+  return region_scratch_bytes(batch, frames, height, width);
+}
+
+int carnator_region_weights(const uint8_t *evidence, int32_t batch, int32_t frames, int32_t height,
+                            int32_t width, int32_t r_active, int32_t r_context, uint8_t *region,
+                            float *weight, void *workspace, size_t ws_bytes, hipStream_t stream) {
+  int rc;
+  if (!evidence || !region || !weight)
+    return fail(CARNATOR_E_NULL, "evidence, region and weight must be non-NULL");
+  if (batch < 1 || frames < 1 || height < 1 || width < 1)
+    return fail(CARNATOR_E_SHAPE, "batch, frames, height and width must be >= 1");
+  if ((int64_t)batch * frames * height * width > (int64_t)INT32_MAX)
+    return fail(CARNATOR_E_SHAPE, "batch*frames*height*width exceeds 2^31-1");
+  if (r_active < 0 || r_context < 0 || r_active + r_context > kMaxRegionRadius)
+    return fail(CARNATOR_E_SHAPE, "radii must be >= 0 with r_active + r_context <= %d",
+                kMaxRegionRadius);
+  if (region_frame_lds(height, width) > kMaxRegionFrameLds)
+    return fail(CARNATOR_E_UNSUPPORTED, "a frame of %d x %d tokens exceeds %d tokens", height, width,
+                (int)(kMaxRegionFrameLds / 2));
+  if ((rc = check_ws(workspace, ws_bytes,
+                     carnator_region_weights_workspace_size(batch, frames, height, width))))
+    return rc;
+  if (reinterpret_cast<uintptr_t>(weight) % 4 != 0)
+    return fail(CARNATOR_E_ALIGN, "weight must be 4-byte aligned");
+  hipError_t e = launch_regions(evidence, batch, frames, height, width, r_active, r_context, region,
+                                weight, workspace, stream);
+  if (e != hipSuccess) return hip_fail(e, "regions");
+  return ok();
+}
+
+int carnator_latent_fusion(const float *z_target, const float *z_hist, const float *weight,
+                           float *z_out, int32_t batch, int32_t channels, int32_t frames,
+                           int32_t height, int32_t width, int32_t patch_t, int32_t patch_h,
+                           int32_t patch_w, hipStream_t stream) {
+  if (!z_target || !z_hist || !weight || !z_out)
+    return fail(CARNATOR_E_NULL, "z_target, z_hist, weight and z_out must be non-NULL");
+  if (batch < 1 || channels < 1 || frames < 1 || height < 1 || width < 1)
+    return fail(CARNATOR_E_SHAPE, "batch, channels, frames, height and width must be >= 1");
+  if (patch_t < 1 || patch_h < 1 || patch_w < 1 || frames % patch_t || height % patch_h ||
+      width % patch_w)
+    return fail(CARNATOR_E_SHAPE, "patch sizes must be >= 1 and divide frames, height and width");
+  if ((reinterpret_cast<uintptr_t>(z_target) | reinterpret_cast<uintptr_t>(z_hist) |
+       reinterpret_cast<uintptr_t>(z_out) | reinterpret_cast<uintptr_t>(weight)) % 4)
+    return fail(CARNATOR_E_ALIGN, "latents and weight must be 4-byte aligned");
+  hipError_t e = launch_fusion(z_target, z_hist, weight, z_out, batch, channels, frames, height,
+                               width, patch_t, patch_h, patch_w, stream);
+  if (e != hipSuccess) return hip_fail(e, "fusion");
+  return ok();
+}
+
+int carnator_region_block_flags(const uint8_t *region, int32_t n_text, const carnator_shape *s,
+                                uint8_t *active_q, uint8_t *context_k, hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if (!region || !active_q || !context_k)
+    return fail(CARNATOR_E_NULL, "region, active_q and context_k must be non-NULL");
+  if (n_text < 0 || n_text >= s->seq_len)
+    return fail(CARNATOR_E_SHAPE, "n_text must be in [0, seq_len) (got %d)", n_text);
+  hipError_t e = launch_block_flags(region, s->batch, n_text, s->seq_len, s->block, active_q,
+                                    context_k, stream);
+  if (e != hipSuccess) return hip_fail(e, "block_flags");
+  return ok();
+}
+
+int carnator_compact_block_mask_bits_region(const uint64_t *bits, const carnator_shape *s,
+                                            const uint8_t *active_q, const uint8_t *context_k,
+                                            int32_t *row_ptr, int32_t *col_idx, int32_t *order,
+                                            int32_t *n_active, void *workspace, size_t ws_bytes,
+                                            hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if (!bits || !active_q || !context_k || !row_ptr || !col_idx || !order || !n_active)
+    return fail(CARNATOR_E_NULL,
+                "bits, active_q, context_k, row_ptr, col_idx, order and n_active must be non-NULL");
+  if (reinterpret_cast<uintptr_t>(bits) % 8 != 0)
+    return fail(CARNATOR_E_ALIGN, "bits must be 8-byte aligned");
+  if ((rc = check_ws(workspace, ws_bytes, carnator_compact_block_mask_bits_workspace_size(s))))
+    return rc;
+  hipError_t e = launch_compact_bits(bits, s->batch, s->heads, n_blocks(s), active_q, context_k,
+                                     true, row_ptr, col_idx, order, n_active, workspace, stream);
+  if (e != hipSuccess) return hip_fail(e, "compact_bits_region");
   return ok();
 }
 
@@ -310,16 +404,16 @@ int carnator_block_sparse_attn(const carnator_view *q, const carnator_view *k,
   if (e != hipSuccess) return hip_fail(e, "compact");
   e = launch_bsattn(to_view(q), to_view(k), to_view(v), static_cast<uint16_t *>(out), osb, osh, osn,
                     s->batch, s->heads, s->seq_len, s->head_dim, s->block, row_ptr, col_idx, order,
-                    sc, lse, stream);
+                    nullptr, sc, lse, stream);
   if (e != hipSuccess) return hip_fail(e, "bsattn");
   return ok();
 }
 
-int carnator_block_sparse_attn_lists(const carnator_view *q, const carnator_view *k,
-                                     const carnator_view *v, void *out, int64_t osb, int64_t osh,
-                                     int64_t osn, const carnator_shape *s, const int32_t *row_ptr,
-                                     const int32_t *col_idx, const int32_t *order, float scale,
-                                     float *lse, hipStream_t stream) {
+// The attention from lists behind both entry points; n_rows NULL walks all rows.
+static int attn_lists(const carnator_view *q, const carnator_view *k, const carnator_view *v,
+                      void *out, int64_t osb, int64_t osh, int64_t osn, const carnator_shape *s,
+                      const int32_t *row_ptr, const int32_t *col_idx, const int32_t *order,
+                      const int32_t *n_rows, float scale, float *lse, hipStream_t stream) {
   int rc;
   if ((rc = check_shape(s))) return rc;
   if ((rc = check_view(q, s, "q"))) return rc;
@@ -335,9 +429,29 @@ int carnator_block_sparse_attn_lists(const carnator_view *q, const carnator_view
   const float sc = scale > 0.f ? scale : (float)(1.0 / sqrt((double)s->head_dim));
   hipError_t e = launch_bsattn(to_view(q), to_view(k), to_view(v), static_cast<uint16_t *>(out), osb, osh,
                                osn, s->batch, s->heads, s->seq_len, s->head_dim, s->block, row_ptr,
-                               col_idx, order, sc, lse, stream);
+                               col_idx, order, n_rows, sc, lse, stream);
   if (e != hipSuccess) return hip_fail(e, "bsattn");
   return ok();
+}
+
+int carnator_block_sparse_attn_lists(const carnator_view *q, const carnator_view *k,
+                                     const carnator_view *v, void *out, int64_t osb, int64_t osh,
+                                     int64_t osn, const carnator_shape *s, const int32_t *row_ptr,
+                                     const int32_t *col_idx, const int32_t *order, float scale,
+                                     float *lse, hipStream_t stream) {
+  return attn_lists(q, k, v, out, osb, osh, osn, s, row_ptr, col_idx, order, nullptr, scale, lse,
+                    stream);
+}
+
+int carnator_block_sparse_attn_rows(const carnator_view *q, const carnator_view *k,
+                                    const carnator_view *v, void *out, int64_t osb, int64_t osh,
+                                    int64_t osn, const carnator_shape *s, const int32_t *row_ptr,
+                                    const int32_t *col_idx, const int32_t *order,
+                                    const int32_t *n_rows, float scale, float *lse,
+                                    hipStream_t stream) {
+  if (!n_rows) return fail(CARNATOR_E_NULL, "n_rows is NULL");
+  return attn_lists(q, k, v, out, osb, osh, osn, s, row_ptr, col_idx, order, n_rows, scale, lse,
+                    stream);
 }
 
 // ---------------------------------------------------------------- signature scan

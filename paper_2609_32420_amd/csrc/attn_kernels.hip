@@ -140,11 +140,14 @@ template <int D, int BS, bool WITH_LSE>
 __global__ void __launch_bounds__(2 * BS, (D == 64 && !WITH_LSE) ? 3 : 2)
 bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, int64_t osh,
               int64_t osn, int H, int N, int nB, const int32_t *__restrict__ row_ptr,
-              const int32_t *__restrict__ col_idx, const int32_t *__restrict__ order, float c2,
-              float *__restrict__ lse) {
+              const int32_t *__restrict__ col_idx, const int32_t *__restrict__ order,
+              const int32_t *__restrict__ n_rows, float c2, float *__restrict__ lse) {
   using C = Cfg<D, BS>;
   constexpr int KT = C::KT, MT = C::MT;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
+  // a row subset: only order[0 .. *n_rows) (the whole workgroup, before any
+  // barrier)
+  if (n_rows != nullptr && (int)blockIdx.x >= *n_rows) return;
 
   // rows, list extents and block indices are clamped into range, so that
   // malformed lists cannot reach outside the tensors
@@ -510,8 +513,8 @@ bsattn_kernel(View q, View k, View v, uint16_t *__restrict__ out, int64_t osb, i
 
 hipError_t launch_bsattn(View q, View k, View v, uint16_t *out, int64_t osb, int64_t osh,
                          int64_t osn, int B, int H, int N, int d, int bs, const int32_t *row_ptr,
-                         const int32_t *col_idx, const int32_t *order, float scale, float *lse,
-                         hipStream_t s) {
+                         const int32_t *col_idx, const int32_t *order, const int32_t *n_rows,
+                         float scale, float *lse, hipStream_t s) {
   const int nB = (N + bs - 1) / bs;
   const unsigned R = (unsigned)B * H * nB;
   const float c2 = scale * 1.4426950408889634f;
@@ -523,7 +526,7 @@ hipError_t launch_bsattn(View q, View k, View v, uint16_t *out, int64_t osb, int
                             hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);                  \
     if (e != hipSuccess) return e;                                                                \
     hipLaunchKernelGGL((bsattn_kernel<DD, BB, LL>), dim3(R), dim3(C::NT), C::LDS, s, q, k, v,     \
-                       out, osb, osh, osn, H, N, nB, row_ptr, col_idx, order, c2, lse);           \
+                       out, osb, osh, osn, H, N, nB, row_ptr, col_idx, order, n_rows, c2, lse);   \
   } while (0)
 #define CARNATOR_BSATTN(DD, BB)                  \
   do {                                           \

@@ -135,38 +135,53 @@ __global__ void __launch_bounds__(256) fill_ones_bits_kernel(uint64_t *__restric
   bits[x] = valid_bits((int)(x % nw), nB, nw);
 }
 
-// Word c of row r after the widening: all valid bits when the row's query
-// block is target-specific, OR the packed dense-column word of its batch
-// entry (colw [B][nw], or NULL).  HnB = H nB rows per batch entry.
+// Word c of row r as the call reads it (HnB = H nB rows per batch entry;
+// rows uint8 [B][nB] and colw, packed column flags [B][nw], may be NULL).
+// Widening: all valid bits when the row's query block is flagged, OR the
+// column word.  Restriction (narrow): AND the column word (context key
+// blocks); whether the row is kept at all is row_kept's.
 __device__ inline uint64_t merged_word(const uint64_t *__restrict__ bits, int r, int c, int nB,
                                        int nw, int HnB, const uint8_t *__restrict__ rows,
-                                       const uint64_t *__restrict__ colw) {
+                                       const uint64_t *__restrict__ colw, bool narrow) {
   uint64_t w = bits[(int64_t)r * nw + c];
   if (rows != nullptr || colw != nullptr) {
     const int b = r / HnB;
-    if (rows != nullptr && rows[(int64_t)b * nB + r % nB] != 0) w = ~0ull;
-    if (colw != nullptr) w |= colw[(int64_t)b * nw + c];
+    if (narrow) {
+      if (colw != nullptr) w &= colw[(int64_t)b * nw + c];
+    } else {
+      if (rows != nullptr && rows[(int64_t)b * nB + r % nB] != 0) w = ~0ull;
+      if (colw != nullptr) w |= colw[(int64_t)b * nw + c];
+    }
   }
   return w & valid_bits(c, nB, nw);
 }
 
+// Whether row r takes part: always when widening, else when its query block
+// is active.
+__device__ inline bool row_kept(int r, int nB, int HnB, const uint8_t *__restrict__ rows,
+                                bool narrow) {
+  return !narrow || rows == nullptr || rows[(int64_t)(r / HnB) * nB + r % nB] != 0;
+}
+
 // G lanes per row (G a power of two >= nw), 64 / G rows per wave: list
-// lengths as popcounts summed over each row's lanes.
+// lengths as popcounts summed over each row's lanes; -1 for a row a
+// restriction leaves out.
 template <int G>
 __global__ void __launch_bounds__(256) count_bits_kernel(const uint64_t *__restrict__ bits, int R,
                                                          int nB, int HnB,
                                                          const uint8_t *__restrict__ rows,
                                                          const uint64_t *__restrict__ colw,
-                                                         int32_t *__restrict__ len) {
+                                                         bool narrow, int32_t *__restrict__ len) {
   const int lane = threadIdx.x & 63;
   const int64_t r = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * (64 / G) + lane / G;
   const int c = lane % G;
   const int nw = (nB + 63) / 64;
+  const bool kept = r < R && row_kept((int)r, nB, HnB, rows, narrow);
   int n = 0;
-  if (r < R && c < nw) n = __popcll(merged_word(bits, (int)r, c, nB, nw, HnB, rows, colw));
+  if (kept && c < nw) n = __popcll(merged_word(bits, (int)r, c, nB, nw, HnB, rows, colw, narrow));
 #pragma unroll
   for (int o = 1; o < G; o <<= 1) n += __shfl_xor(n, o);
-  if (r < R && c == 0) len[r] = n;
+  if (r < R && c == 0) len[r] = kept ? n : -1;
 }
 
 // One wave per row: ascending kept key blocks at col_idx[row_ptr[r] ...].
@@ -176,13 +191,15 @@ __global__ void __launch_bounds__(256) fill_bits_kernel(const uint64_t *__restri
                                                         int nB, int HnB,
                                                         const uint8_t *__restrict__ rows,
                                                         const uint64_t *__restrict__ colw,
+                                                        bool narrow,
                                                         const int32_t *__restrict__ row_ptr,
                                                         int32_t *__restrict__ col_idx) {
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (r >= R) return;
+  if (r >= R || !row_kept((int)r, nB, HnB, rows, narrow)) return;
   const int nw = (nB + 63) / 64;
-  const uint64_t mine = lane < nw ? merged_word(bits, (int)r, lane, nB, nw, HnB, rows, colw) : 0ull;
+  const uint64_t mine =
+      lane < nw ? merged_word(bits, (int)r, lane, nB, nw, HnB, rows, colw, narrow) : 0ull;
   const uint64_t below = (1ull << lane) - 1ull;
   int pos = row_ptr[r];
   for (int c = 0; c < nw; ++c) {
@@ -244,18 +261,23 @@ constexpr size_t kCountSortLds = 152 * 1024;
 //     per key bit, each takes its group's next slot plus its rank among those
 //     lanes, and the lowest of them advances the counter.  Lengths descend,
 //     waves and rows ascend: the order the oracle defines.
-// LDS: uint32 counters [nB + 1][16] (index (nB - L) 16 + w), then with
-// LEN_LDS the lengths as uint16 [R]; otherwise they are read from len_g.
+// A length of -1 marks a row left out of a restricted call: its list is
+// empty and it sorts after every row of length >= 0 (key nB + 1), in row
+// order; *n_active (when not NULL) receives the number of the other rows,
+// which the exclusive scan leaves as the first slot of key nB + 1.
+// LDS: uint32 counters [nB + 2][16] (index (nB - L) 16 + w), then with
+// LEN_LDS the lengths as int16 [R]; otherwise they are read from len_g.
 template <bool LEN_LDS>
 __global__ void __launch_bounds__(kScanThreads) count_sort_kernel(const int32_t *__restrict__ len_g,
                                                                   int R, int nB,
                                                                   int32_t *__restrict__ row_ptr,
-                                                                  int32_t *__restrict__ order) {
+                                                                  int32_t *__restrict__ order,
+                                                                  int32_t *__restrict__ n_active) {
   constexpr int kWaves = kScanThreads / 64;
   __shared__ int sh[kWaves];
   extern __shared__ uint32_t cnt[];
-  const int K = (nB + 1) * kWaves;
-  uint16_t *len16 = reinterpret_cast<uint16_t *>(cnt + K);
+  const int K = (nB + 2) * kWaves;
+  int16_t *len16 = reinterpret_cast<int16_t *>(cnt + K);
   const int t = threadIdx.x, lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   for (int i = t; i < K; i += kScanThreads) cnt[i] = 0;
@@ -271,7 +293,7 @@ __global__ void __launch_bounds__(kScanThreads) count_sort_kernel(const int32_t 
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int r = r0 + u * kScanThreads + t;
-        if (r < R) len16[r] = (uint16_t)v[u];
+        if (r < R) len16[r] = (int16_t)v[u];
       }
     }
   }
@@ -288,7 +310,7 @@ __global__ void __launch_bounds__(kScanThreads) count_sort_kernel(const int32_t 
     int part = 0;
     for (int r0 = rlo; r0 < rhi; r0 += 64) {
       const int r = r0 + lane;
-      part += r < rhi ? lenv(r) : 0;
+      part += r < rhi ? max(lenv(r), 0) : 0;
     }
     const int wtot = __builtin_amdgcn_readlane(wave_incl_scan(part), 63);
     if (lane == 0) sh[w] = wtot;
@@ -301,7 +323,7 @@ __global__ void __launch_bounds__(kScanThreads) count_sort_kernel(const int32_t 
     }
     for (int r0 = rlo; r0 < rhi; r0 += 64) {
       const int r = r0 + lane;
-      const int v = r < rhi ? lenv(r) : 0;
+      const int v = r < rhi ? max(lenv(r), 0) : 0;
       const int incl = wave_incl_scan(v);
       if (r < rhi) row_ptr[r] = off + incl - v;
       off += __builtin_amdgcn_readlane(incl, 63);
@@ -311,13 +333,13 @@ __global__ void __launch_bounds__(kScanThreads) count_sort_kernel(const int32_t 
 
   // ---- order
   int kbits = 0;
-  while ((1 << kbits) <= nB) ++kbits;
-  // the lanes of this walk step holding the same length as this lane
-  auto peers_of = [&](bool on, int L) __attribute__((always_inline)) {
+  while ((1 << kbits) <= nB + 1) ++kbits;
+  // the lanes of this walk step holding the same key (nB - length) as this lane
+  auto peers_of = [&](bool on, int key) __attribute__((always_inline)) {
     unsigned long long m = __ballot(on);
     for (int b = 0; b < kbits; ++b) {
-      const unsigned long long ones = __ballot(on && ((L >> b) & 1));
-      m &= ((L >> b) & 1) ? ones : ~ones;
+      const unsigned long long ones = __ballot(on && ((key >> b) & 1));
+      m &= ((key >> b) & 1) ? ones : ~ones;
     }
     return m;
   };
@@ -342,13 +364,16 @@ __global__ void __launch_bounds__(kScanThreads) count_sort_kernel(const int32_t 
     }
   }
   __syncthreads();
+  // (wave 0 reads the slot before its own pass-2 updates; other waves never
+  // update counter (nB + 1) 16 + 0)
+  if (t == 0 && n_active != nullptr) *n_active = (int32_t)cnt[(nB + 1) * kWaves];
   for (int r0 = rlo; r0 < rhi; r0 += 64) {
     const int r = r0 + lane;
     const bool on = r < rhi;
-    const int L = on ? lenv(r) : 0;
-    const unsigned long long m = peers_of(on, L);
+    const int key = on ? nB - lenv(r) : 0;
+    const unsigned long long m = peers_of(on, key);
     if (on) {
-      uint32_t &c = cnt[(nB - L) * kWaves + w];
+      uint32_t &c = cnt[key * kWaves + w];
       order[(int)c + __popcll(m & ((1ull << lane) - 1ull))] = r;
       // every lane of the group has read the counter before the lowest lane
       // writes it back (one wave: its LDS accesses complete in program order)
@@ -371,22 +396,22 @@ size_t compact_scratch_bytes(int64_t R) { return align_up((size_t)R * sizeof(int
 
 // row_ptr and order from the list lengths (one workgroup).
 static hipError_t launch_sort(const int32_t *len, int64_t R, int nB, int32_t *row_ptr, int32_t *order,
-                       hipStream_t s) {
-  const size_t cnt_lds = (size_t)(nB + 1) * (kScanThreads / 64) * sizeof(uint32_t);
-  const size_t len_lds = (size_t)R * sizeof(uint16_t);
+                              int32_t *n_active, hipStream_t s) {
+  const size_t cnt_lds = (size_t)(nB + 2) * (kScanThreads / 64) * sizeof(uint32_t);
+  const size_t len_lds = (size_t)R * sizeof(int16_t);
   hipError_t e;
   if (cnt_lds + len_lds <= kCountSortLds) {
     e = hipFuncSetAttribute(reinterpret_cast<const void *>(&count_sort_kernel<true>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)(cnt_lds + len_lds));
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(count_sort_kernel<true>, dim3(1), dim3(kScanThreads), cnt_lds + len_lds, s,
-                       len, (int)R, nB, row_ptr, order);
+                       len, (int)R, nB, row_ptr, order, n_active);
   } else {
     e = hipFuncSetAttribute(reinterpret_cast<const void *>(&count_sort_kernel<false>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)cnt_lds);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(count_sort_kernel<false>, dim3(1), dim3(kScanThreads), cnt_lds, s, len,
-                       (int)R, nB, row_ptr, order);
+                       (int)R, nB, row_ptr, order, n_active);
   }
   return hipGetLastError();
 }
@@ -404,7 +429,7 @@ hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_p
     else hipLaunchKernelGGL(KERNEL<32>, dim3(g), dim3(256), 0, s, __VA_ARGS__);          \
   } while (0)
   CARNATOR_ROWS(count_kernel, mask, R, nB, len);
-  hipError_t e = launch_sort(len, R, nB, row_ptr, order, s);
+  hipError_t e = launch_sort(len, R, nB, row_ptr, order, nullptr, s);
   if (e != hipSuccess) return e;
   CARNATOR_ROWS(fill_kernel, mask, R, nB, row_ptr, col_idx);
   return hipGetLastError();
@@ -437,14 +462,15 @@ size_t compact_bits_scratch_bytes(int64_t R, int B, int nB) {
 }
 
 hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const uint8_t *rows,
-                               const uint8_t *cols, int32_t *row_ptr, int32_t *col_idx,
-                               int32_t *order, void *scratch, hipStream_t s) {
+                               const uint8_t *cols, bool narrow, int32_t *row_ptr,
+                               int32_t *col_idx, int32_t *order, int32_t *n_active, void *scratch,
+                               hipStream_t s) {
   const int64_t R = (int64_t)B * H * nB;
   int32_t *len = static_cast<int32_t *>(scratch);
   uint64_t *colw = nullptr;
   hipError_t e;
   if (cols != nullptr) {
-    // the dense-column flags of each batch entry, packed once like a mask row
+    // the column flags of each batch entry, packed once like a mask row
     colw = reinterpret_cast<uint64_t *>(static_cast<char *>(scratch) + compact_scratch_bytes(R));
     if ((e = launch_pack(cols, B, nB, colw, s)) != hipSuccess) return e;
   }
@@ -457,15 +483,15 @@ hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const
 #define CARNATOR_G(GG)                                                                            \
   case GG:                                                                                        \
     hipLaunchKernelGGL(count_bits_kernel<GG>, dim3(gc), dim3(256), 0, s, bits, (int)R, nB, HnB,   \
-                       rows, colw, len);                                                          \
+                       rows, colw, narrow, len);                                                  \
     break;
     CARNATOR_G(1) CARNATOR_G(2) CARNATOR_G(4) CARNATOR_G(8) CARNATOR_G(16) CARNATOR_G(32)
 #undef CARNATOR_G
     default: return hipErrorInvalidValue;
   }
-  if ((e = launch_sort(len, R, nB, row_ptr, order, s)) != hipSuccess) return e;
+  if ((e = launch_sort(len, R, nB, row_ptr, order, n_active, s)) != hipSuccess) return e;
   hipLaunchKernelGGL(fill_bits_kernel, dim3((unsigned)((R + 3) / 4)), dim3(256), 0, s, bits,
-                     (int)R, nB, HnB, rows, colw, row_ptr, col_idx);
+                     (int)R, nB, HnB, rows, colw, narrow, row_ptr, col_idx);
   return hipGetLastError();
 }
 

@@ -109,18 +109,41 @@ hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_p
 hipError_t launch_pack(const uint8_t *mask, int64_t R, int nB, uint64_t *bits, hipStream_t s);
 hipError_t launch_unpack(const uint64_t *bits, int64_t R, int nB, uint8_t *mask, hipStream_t s);
 hipError_t launch_fill_ones_bits(uint64_t *bits, int64_t R, int nB, hipStream_t s);
-// Compaction of the packed mask [B][H][nB] rows widened by rows / cols
-// (uint8 [B][nB] each, or NULL); scratch of compact_bits_scratch_bytes.
+// Compaction of the packed mask [B][H][nB] rows, rows / cols uint8 [B][nB]
+// each or NULL; scratch of compact_bits_scratch_bytes.  Widening (narrow
+// false): flagged rows become full, flagged columns are added.  Restriction
+// (narrow true): only flagged (active) rows and flagged (context) columns
+// are kept; order lists the active rows first and *n_active (if not NULL)
+// receives their number.
 size_t compact_bits_scratch_bytes(int64_t R, int B, int nB);
 hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const uint8_t *rows,
-                               const uint8_t *cols, int32_t *row_ptr, int32_t *col_idx,
-                               int32_t *order, void *scratch, hipStream_t s);
+                               const uint8_t *cols, bool narrow, int32_t *row_ptr,
+                               int32_t *col_idx, int32_t *order, int32_t *n_active, void *scratch,
+                               hipStream_t s);
+
+// ---- region-restricted reuse -------------------------------------------------
+// Region codes (3 evidence, 2 band, 1 context, 0 outside) and the blend
+// weight W over [B][T][H][W] tokens from the evidence; scratch of
+// region_scratch_bytes; LDS of region_frame_lds per frame.
+size_t region_frame_lds(int H, int W);
+size_t region_scratch_bytes(int B, int T, int H, int W);
+hipError_t launch_regions(const uint8_t *evidence, int B, int T, int H, int W, int ra, int rc,
+                          uint8_t *region, float *weight, void *scratch, hipStream_t s);
+// zo = W zt + (1 - W) zh over fp32 latents [B][C][Tl][Hl][Wl], W on the token
+// grid [B][Tl / pt][Hl / ph][Wl / pw].
+hipError_t launch_fusion(const float *zt, const float *zh, const float *weight, float *zo, int B,
+                         int C, int Tl, int Hl, int Wl, int pt, int ph, int pw, hipStream_t s);
+// Active query blocks and context key blocks (uint8 [B][nB]) from the region
+// codes of the video tokens [B][N - n_text]; text tokens count as both.
+hipError_t launch_block_flags(const uint8_t *region, int B, int n_text, int N, int bs, uint8_t *act,
+                              uint8_t *ctx, hipStream_t s);
 
 // ---- attention -------------------------------------------------------------
+// Rows order[0 .. *n_rows) when n_rows is not NULL, else all B H nB rows.
 hipError_t launch_bsattn(View q, View k, View v, uint16_t *out, int64_t osb, int64_t osh,
                          int64_t osn, int B, int H, int N, int d, int bs, const int32_t *row_ptr,
-                         const int32_t *col_idx, const int32_t *order, float scale, float *lse,
-                         hipStream_t s);
+                         const int32_t *col_idx, const int32_t *order, const int32_t *n_rows,
+                         float scale, float *lse, hipStream_t s);
 
 // ---- signature scan ----------------------------------------------------------
 hipError_t launch_sig(const float *query, int64_t nq, const float *bank, int64_t m, int64_t dim,

@@ -1,0 +1,233 @@
+// Region-restricted reuse in the middle layers.
+//
+// Sec. 3.3 ("Region-Guided Latent Reuse"): the Evidence Region grows into an
+// Active Region and a larger Context Region over the T x H x W token grid;
+// every later latent is W * (target-updated latent) + (1 - W) * (historical
+// latent), with W = 1 on the evidence, 1 - smoothstep(normalised Chebyshev
+// distance to the evidence) on the transition band (active minus evidence)
+// and 0 outside the active region.  Appendix C.3: active = evidence dilated
+// by 2 tokens, context = active dilated by 3 more, per latent frame on the
+// H x W grid, the band distance normalised by its maximum over the band.
+// Sec. 3.3 ("Joint Reuse in Intermediate Layers"): only the connectivity of
+// active query blocks to context key blocks is kept (the lists come from
+// compact_kernels.hip).
+//
+// Dilating by a square of radius r is thresholding the Chebyshev distance to
+// the evidence at r (squares compose: radius 2 then 3 is radius 5), so one
+// distance transform per frame gives all three regions and the band
+// distance.  The transform is separable: the distance along the row to the
+// nearest evidence token, then the minimum over the rows within reach of
+// max(|dy|, row distance), capped at r_active + r_context + 1.
+#include "internal.h"
+
+namespace carnator {
+namespace {
+
+constexpr int kRegionThreads = 256;
+
+// One workgroup per (b, t) frame, the frame's evidence and row distances in
+// LDS (2 H W bytes).  Writes the region code (3 evidence, 2 band, 1 context,
+// 0 outside) and the capped distance of every token, and the largest band
+// distance of the frame (0 when it has no band).
+__global__ void __launch_bounds__(kRegionThreads) region_kernel(
+    const uint8_t *__restrict__ evidence, int HW, int W, int ra, int rc,
+    uint8_t *__restrict__ region, uint8_t *__restrict__ dist, int32_t *__restrict__ frame_max) {
+  extern __shared__ uint8_t fr[];
+  uint8_t *ev = fr, *rowd = fr + HW;
+  __shared__ int wmax[kRegionThreads / 64];
+  const int64_t base = (int64_t)blockIdx.x * HW;
+  const int R = ra + rc, cap = R + 1;
+  const int t = threadIdx.x;
+  for (int p = t; p < HW; p += kRegionThreads) ev[p] = evidence[base + p] != 0;
+  __syncthreads();
+  for (int p = t; p < HW; p += kRegionThreads) {
+    const int y = p / W, x = p - y * W;
+    const uint8_t *row = ev + y * W;
+    int d = cap;
+    for (int k = 0; k <= R; ++k) {
+      if ((x - k >= 0 && row[x - k]) || (x + k < W && row[x + k])) {
+        d = k;
+        break;
+      }
+    }
+    rowd[p] = (uint8_t)d;
+  }
+  __syncthreads();
+  const int H = HW / W;
+  int bandmax = 0;
+  for (int p = t; p < HW; p += kRegionThreads) {
+    const int y = p / W, x = p - y * W;
+    int d = rowd[p];
+    for (int k = 1; k <= R && k < d; ++k) {
+      if (y - k >= 0) d = min(d, max(k, (int)rowd[p - k * W]));
+      if (y + k < H) d = min(d, max(k, (int)rowd[p + k * W]));
+    }
+    const uint8_t code = d == 0 ? 3 : d <= ra ? 2 : d <= R ? 1 : 0;
+    region[base + p] = code;
+    dist[base + p] = (uint8_t)d;
+    if (code == 2) bandmax = max(bandmax, d);
+  }
+  // workgroup maximum
+  for (int o = 32; o > 0; o >>= 1) bandmax = max(bandmax, __shfl_xor(bandmax, o));
+  if ((t & 63) == 0) wmax[t >> 6] = bandmax;
+  __syncthreads();
+  if (t == 0) {
+    int m = 0;
+    for (int w = 0; w < kRegionThreads / 64; ++w) m = max(m, wmax[w]);
+    frame_max[blockIdx.x] = m;
+  }
+}
+
+// One thread per token: W from the region code, the distance and the band
+// maximum over the frames of the token's batch entry.
+__global__ void __launch_bounds__(256) weight_kernel(const uint8_t *__restrict__ region,
+                                                     const uint8_t *__restrict__ dist,
+                                                     const int32_t *__restrict__ frame_max,
+                                                     int T, int64_t per_batch, int64_t total,
+                                                     float *__restrict__ weight) {
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (x >= total) return;
+  const int b = (int)(x / per_batch);
+  const uint8_t code = region[x];
+  float w = 0.f;
+  if (code == 3) {
+    w = 1.f;
+  } else if (code == 2) {
+    int m = 1;
+    for (int f = 0; f < T; ++f) m = max(m, frame_max[b * T + f]);
+    const float s = (float)dist[x] / (float)m;
+    w = 1.f - s * s * (3.f - 2.f * s);
+  }
+  weight[x] = w;
+}
+
+// z_out = W z_target + (1 - W) z_hist over latents [B, C, Tl, Hl, Wl], W on
+// the token grid [B, Tl / pt, Hl / ph, Wl / pw].  Four consecutive elements
+// of a row per thread (Wl % 4 == 0, 16-byte aligned tensors: 16-byte loads
+// and stores).  z_out may be z_target or z_hist: each element is read before
+// it is written, by the same thread.
+__global__ void __launch_bounds__(256) fusion4_kernel(const float4 *zt, const float4 *zh,
+                                                      const float *__restrict__ weight,
+                                                      float4 *zo, int64_t quads, int C, int Tl,
+                                                      int Hl, int Wl, int pt, int ph, int pw) {
+  const int64_t qi = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (qi >= quads) return;
+  const int64_t e = qi * 4;
+  const int x0 = (int)(e % Wl);
+  int64_t r = e / Wl;
+  const int y = (int)(r % Hl);
+  r /= Hl;
+  const int tt = (int)(r % Tl);
+  const int b = (int)(r / Tl / C);
+  const int Tg = Tl / pt, Hg = Hl / ph, Wg = Wl / pw;
+  const float *wrow = weight + (((int64_t)b * Tg + tt / pt) * Hg + y / ph) * Wg;
+  const float4 a = zt[qi], h = zh[qi];
+  const float w0 = wrow[x0 / pw], w1 = wrow[(x0 + 1) / pw], w2 = wrow[(x0 + 2) / pw],
+              w3 = wrow[(x0 + 3) / pw];
+  float4 o;
+  o.x = w0 * a.x + (1.f - w0) * h.x;
+  o.y = w1 * a.y + (1.f - w1) * h.y;
+  o.z = w2 * a.z + (1.f - w2) * h.z;
+  o.w = w3 * a.w + (1.f - w3) * h.w;
+  zo[qi] = o;
+}
+
+// The same one element per thread (any Wl, any 4-byte alignment).
+__global__ void __launch_bounds__(256) fusion1_kernel(const float *zt, const float *zh,
+                                                      const float *__restrict__ weight, float *zo,
+                                                      int64_t total, int C, int Tl, int Hl,
+                                                      int Wl, int pt, int ph, int pw) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= total) return;
+  const int x = (int)(e % Wl);
+  int64_t r = e / Wl;
+  const int y = (int)(r % Hl);
+  r /= Hl;
+  const int tt = (int)(r % Tl);
+  const int b = (int)(r / Tl / C);
+  const int Tg = Tl / pt, Hg = Hl / ph, Wg = Wl / pw;
+  const float w = weight[(((int64_t)b * Tg + tt / pt) * Hg + y / ph) * Wg + x / pw];
+  zo[e] = w * zt[e] + (1.f - w) * zh[e];
+}
+
+// One wave per (b, block): a query block is active if one of its tokens is
+// (code >= 2), a key block is context if one of its tokens is (code >= 1);
+// text tokens, before the video tokens, count as both.  Lane l looks at
+// tokens l and l + 64 of the block (blocks are at most 128 tokens).
+__global__ void __launch_bounds__(256) block_flags_kernel(const uint8_t *__restrict__ region,
+                                                          int n_text, int N, int bs, int nB,
+                                                          int64_t total, uint8_t *__restrict__ act,
+                                                          uint8_t *__restrict__ ctx) {
+  const int64_t g = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (g >= total) return;
+  const int b = (int)(g / nB), i = (int)(g - (int64_t)b * nB);
+  const int nv = N - n_text;
+  int best = 0;
+  for (int u = 0; u < 2; ++u) {
+    const int off = u * 64 + lane;
+    const int tok = i * bs + off;
+    if (off < bs && tok < N)
+      best = max(best, tok < n_text ? 3 : (int)region[(int64_t)b * nv + (tok - n_text)]);
+  }
+  const bool a = __ballot(best >= 2) != 0, c = __ballot(best >= 1) != 0;
+  if (lane == 0) {
+    act[g] = a ? 1 : 0;
+    ctx[g] = c ? 1 : 0;
+  }
+}
+
+}  // namespace
+
+size_t region_frame_lds(int H, int W) { return (size_t)2 * H * W; }
+
+size_t region_scratch_bytes(int B, int T, int H, int W) {
+  return align_up((size_t)B * T * H * W) + align_up((size_t)B * T * sizeof(int32_t));
+}
+
+hipError_t launch_regions(const uint8_t *evidence, int B, int T, int H, int W, int ra, int rc,
+                          uint8_t *region, float *weight, void *scratch, hipStream_t s) {
+  const int HW = H * W;
+  uint8_t *dist = static_cast<uint8_t *>(scratch);
+  int32_t *fmax = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) +
+                                              align_up((size_t)B * T * HW));
+  const size_t lds = region_frame_lds(H, W);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&region_kernel),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(region_kernel, dim3((unsigned)(B * T)), dim3(kRegionThreads), lds, s,
+                     evidence, HW, W, ra, rc, region, dist, fmax);
+  const int64_t per = (int64_t)T * HW, total = (int64_t)B * per;
+  hipLaunchKernelGGL(weight_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, region,
+                     dist, fmax, T, per, total, weight);
+  return hipGetLastError();
+}
+
+hipError_t launch_fusion(const float *zt, const float *zh, const float *weight, float *zo, int B,
+                         int C, int Tl, int Hl, int Wl, int pt, int ph, int pw, hipStream_t s) {
+  const int64_t total = (int64_t)B * C * Tl * Hl * Wl;
+  if (total == 0) return hipSuccess;
+  const bool vec = Wl % 4 == 0 && ((reinterpret_cast<uintptr_t>(zt) | reinterpret_cast<uintptr_t>(zh) |
+                                    reinterpret_cast<uintptr_t>(zo)) % 16) == 0;
+  if (vec) {
+    const int64_t quads = total / 4;
+    hipLaunchKernelGGL(fusion4_kernel, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, s,
+                       reinterpret_cast<const float4 *>(zt), reinterpret_cast<const float4 *>(zh),
+                       weight, reinterpret_cast<float4 *>(zo), quads, C, Tl, Hl, Wl, pt, ph, pw);
+  } else {
+    hipLaunchKernelGGL(fusion1_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, zt,
+                       zh, weight, zo, total, C, Tl, Hl, Wl, pt, ph, pw);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_block_flags(const uint8_t *region, int B, int n_text, int N, int bs, uint8_t *act,
+                              uint8_t *ctx, hipStream_t s) {
+  const int nB = (N + bs - 1) / bs;
+  const int64_t total = (int64_t)B * nB;
+  hipLaunchKernelGGL(block_flags_kernel, dim3((unsigned)((total + 3) / 4)), dim3(256), 0, s, region,
+                     n_text, N, bs, nB, total, act, ctx);
+  return hipGetLastError();
+}
+
+}  // namespace carnator

@@ -208,3 +208,36 @@ def test_bit_packed_workspace_size(L):
     assert L.carnator_compact_block_mask_bits_workspace_size(ctypes.byref(s)) == 12288 + 256
     assert L.carnator_compact_block_mask_bits_workspace_size(ctypes.byref(_shape(d=96))) == 0
     assert R * 4 == 12288
+
+
+def test_region_entry_points_reject(L):
+    p = ctypes.c_void_p(0x1000)
+    ws = ctypes.c_void_p(0x40000)
+    rw = L.carnator_region_weights
+    assert rw(None, 1, 2, 8, 8, 2, 3, p, p, ws, 1 << 20, None) == -1
+    assert rw(p, 0, 2, 8, 8, 2, 3, p, p, ws, 1 << 20, None) == -2
+    assert rw(p, 1, 2, 8, 8, -1, 3, p, p, ws, 1 << 20, None) == -2
+    assert rw(p, 1, 2, 8, 8, 200, 51, p, p, ws, 1 << 20, None) == -2
+    assert rw(p, 1, 2, 300, 300, 2, 3, p, p, ws, 1 << 30, None) == -3
+    assert rw(p, 1, 2, 8, 8, 2, 3, p, p, ws, 16, None) == -5
+    assert rw(p, 1, 2, 8, 8, 2, 3, p, ctypes.c_void_p(0x1002), ws, 1 << 20, None) == -4
+    assert L.carnator_region_weights_workspace_size(1, 2, 8, 8) >= 2 * 64 + 2 * 4
+    assert L.carnator_region_weights_workspace_size(0, 2, 8, 8) == 0
+    lf = L.carnator_latent_fusion
+    assert lf(p, p, p, None, 1, 16, 4, 8, 8, 1, 2, 2, None) == -1
+    assert lf(p, p, p, p, 1, 16, 4, 8, 8, 1, 3, 2, None) == -2
+    assert lf(p, p, p, p, 1, 16, 4, 8, 8, 0, 2, 2, None) == -2
+    assert lf(p, ctypes.c_void_p(0x1001), p, p, 1, 16, 4, 8, 8, 1, 2, 2, None) == -4
+    s = _shape(1, 1, 200, 64, 64)
+    bf = L.carnator_region_block_flags
+    assert bf(None, 0, ctypes.byref(s), p, p, None) == -1
+    assert bf(p, 200, ctypes.byref(s), p, p, None) == -2
+    assert bf(p, -1, ctypes.byref(s), p, p, None) == -2
+    cr = L.carnator_compact_block_mask_bits_region
+    assert cr(p, ctypes.byref(s), p, p, p, p, p, None, ws, 1 << 20, None) == -1
+    assert cr(p, ctypes.byref(s), None, p, p, p, p, p, ws, 1 << 20, None) == -1
+    assert cr(p, ctypes.byref(s), p, p, p, p, p, p, ws, 4, None) == -5
+    q = _view()
+    ar = L.carnator_block_sparse_attn_rows
+    assert ar(ctypes.byref(q), ctypes.byref(q), ctypes.byref(q), ctypes.c_void_p(0x20000), 0, 0, 64,
+              ctypes.byref(_shape()), p, p, p, None, 0.0, None, None) == -1
