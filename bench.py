@@ -22,6 +22,12 @@ copy of known size (paper_2609_32420_amd/measured_traffic.json); it is null
 when the kernel source no longer matches the one those counters were taken
 on.
 
+``region_restricted`` (after the timed region, skipped with --no-region):
+the middle-layer variant -- regions and blend weight from an evidence
+region, the latent blend (HBM-bound; its GB/s against the 8 TB/s peak),
+block flags, compaction restricted to active rows and context keys, and
+the attention of the active rows only -- each timed alone.
+
 ``mask_bank`` (after the timed region, skipped with --no-bank): the same
 masks in their stored, bit-packed form -- the builder writing a bank slot
 directly, compaction of a slot with the widening applied while reading, and
@@ -163,6 +169,92 @@ def bank_pass(P, torch, stream, sets, flags, masks, lists, ws_mask, wl, steps):
     }
 
 
+LATENT_CHANNELS, LATENT_PATCH = 16, (1, 2, 2)
+
+
+def region_pass(P, torch, stream, sets, wl, steps):
+    """The region-restricted middle-layer path on the same inputs, after the
+    timed region: regions and W from a seeded evidence region, the latent
+    blend over a 16-channel latent twice as fine as the token grid in H and
+    W, block flags, compaction of the stored mask restricted to active rows
+    and context keys, and the attention of the active rows only.  Each call
+    timed alone between two events."""
+    import synth
+    B, H, nb, N, d, bs = wl.batch, wl.heads, wl.n_blocks, wl.seq_len, wl.head_dim, wl.block
+    dev = sets[0][0]["q"].device
+    ev = [torch.as_tensor(synth.evidence_region(wl, seed=i), device=dev) for i in range(len(sets))]
+    zs = [synth.latents(wl, LATENT_CHANNELS, LATENT_PATCH, seed=i, device=dev) for i in range(len(sets))]
+    zout = torch.empty_like(zs[0][0])
+    T, Hg, Wg = wl.grid
+    region = (torch.empty(B, T, Hg, Wg, dtype=torch.uint8, device=dev),
+              torch.empty(B, T, Hg, Wg, dtype=torch.float32, device=dev))
+    ws_reg = torch.empty(max(P.lib().carnator_region_weights_workspace_size(B, T, Hg, Wg), 1), dtype=torch.uint8,
+                         device=dev)
+    flags = (torch.empty(B, nb, dtype=torch.uint8, device=dev), torch.empty(B, nb, dtype=torch.uint8, device=dev))
+    slots = [P.build_block_mask_bits(x["q_hist"], x["k_hist"], bs, wl.tau) for x, _ in sets]
+    ws_cb = P.compact_block_mask_bits_workspace(slots[0])
+    R = B * H * nb
+    lists = (torch.empty(R + 1, dtype=torch.int32, device=dev), torch.empty(R * nb, dtype=torch.int32, device=dev),
+             torch.empty(R, dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev))
+    outs = [torch.empty(B, H, N, d, dtype=torch.bfloat16, device=dev) for _ in sets]
+    names = ("regions", "fusion", "flags", "compact", "attn")
+    t = {k: [] for k in names}
+    used = []
+    for i in range(steps + 1):
+        si = i % len(sets)
+        x = sets[si][0]
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        e[0].record(stream)
+        P.region_weights(ev[si], 2, 3, out=region, workspace=ws_reg)
+        e[1].record(stream)
+        P.latent_fusion(zs[si][0], zs[si][1], region[1], out=zout)
+        e[2].record(stream)
+        P.region_block_flags(region[0], wl.n_text, bs, out=flags)
+        e[3].record(stream)
+        P.compact_block_mask_bits_region(slots[si], flags[0], flags[1], out=lists, workspace=ws_cb)
+        e[4].record(stream)
+        P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists[:3], bs, out=outs[si], n_rows=lists[3])
+        e[5].record(stream)
+        if i == 0:
+            continue
+        used.append(si)
+        for k, a in zip(names, range(5)):
+            t[k].append((e[a], e[a + 1]))
+    torch.cuda.synchronize()
+    ms = {k: [a.elapsed_time(b) for a, b in v] for k, v in t.items()}
+    # executed attention work of each set's restricted mask (untimed)
+    shifts = torch.arange(64, device=dev, dtype=torch.int64)
+    per_set = []
+    for si in range(len(sets)):
+        P.region_weights(ev[si], 2, 3, out=region, workspace=ws_reg)
+        P.region_block_flags(region[0], wl.n_text, bs, out=flags)
+        m = ((slots[si][..., :, None] >> shifts) & 1).reshape(B, H, nb, -1)[..., :nb].bool()
+        m &= flags[0].bool()[:, None, :, None] & flags[1].bool()[:, None, None, :]
+        per_set.append({"flops": executed_flops(m.to(torch.uint8).cpu().numpy(), N, bs, d),
+                        "active_q": int(flags[0].sum().item()), "context_k": int(flags[1].sum().item()),
+                        "evidence": float(ev[si].float().mean().item())})
+    fl_total = sum(per_set[si]["flops"] for si in used)
+    attn_s = sum(ms["attn"]) * 1e-3
+    ms = {k: float(np.mean(v)) for k, v in ms.items()}
+    zbytes = 3.0 * zs[0][0].numel() * 4 + region[1].numel() * 4
+    return {
+        "evidence_fraction": [round(p_["evidence"], 4) for p_ in per_set],
+        "active_query_blocks": [p_["active_q"] for p_ in per_set],
+        "context_key_blocks": [p_["context_k"] for p_ in per_set],
+        "n_blocks": nb, "heads": H,
+        "latent": [B, LATENT_CHANNELS, T * LATENT_PATCH[0], Hg * LATENT_PATCH[1], Wg * LATENT_PATCH[2]],
+        "regions_ms_per_call": round(ms["regions"], 4),
+        "fusion_ms_per_call": round(ms["fusion"], 4),
+        "fusion_GBps": round(zbytes / (ms["fusion"] * 1e-3) / 1e9, 1),
+        "fusion_pct_hbm_peak": round(100.0 * zbytes / (ms["fusion"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 2),
+        "flags_ms_per_call": round(ms["flags"], 4),
+        "compact_ms_per_call": round(ms["compact"], 4),
+        "attn_rows_ms_per_call": round(ms["attn"], 4),
+        "attn_rows_executed_tflop_per_call": round(fl_total / len(used) / 1e12, 4),
+        "attn_rows_executed_tflops": round(fl_total / attn_s / 1e12, 2),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -172,6 +264,7 @@ def main():
     ap.add_argument("--sets", type=int, default=3, help="input sets rotated across steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bank", action="store_true", help="skip the bit-packed mask bank pass")
+    ap.add_argument("--no-region", action="store_true", help="skip the region-restricted pass")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before timing, copy a buffer of this size once (a reference kernel of known "
                          "traffic for hardware byte counters)")
@@ -272,6 +365,7 @@ def main():
 
     bank = None if args.no_bank else bank_pass(P, torch, stream, sets, flags, masks, lists, ws_mask, wl,
                                                 args.steps)
+    region = None if args.no_region else region_pass(P, torch, stream, sets, wl, args.steps)
 
     # algorithmic work of one step (averaged over the rotated sets)
     fl_exec = float(np.mean([executed_flops(m.cpu().numpy(), N, bs, d) for m in masks]))
@@ -322,6 +416,8 @@ def main():
     }
     if bank is not None:
         res["mask_bank"] = bank
+    if region is not None:
+        res["region_restricted"] = region
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(wl)

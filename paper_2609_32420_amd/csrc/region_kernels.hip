@@ -23,10 +23,11 @@
 namespace carnator {
 namespace {
 
-constexpr int kRegionThreads = 256;
+constexpr int kRegionThreads = 1024;
 
-// One workgroup per (b, t) frame, the frame's evidence and row distances in
-// LDS (2 H W bytes).  Writes the region code (3 evidence, 2 band, 1 context,
+// One workgroup of 1024 threads per (b, t) frame (few frames, each thread a
+// handful of tokens), the frame's evidence and row distances in LDS
+// (2 H W bytes).  Writes the region code (3 evidence, 2 band, 1 context,
 // 0 outside) and the capped distance of every token, and the largest band
 // distance of the frame (0 when it has no band).
 __global__ void __launch_bounds__(kRegionThreads) region_kernel(
@@ -105,25 +106,33 @@ __global__ void __launch_bounds__(256) weight_kernel(const uint8_t *__restrict__
 // the token grid [B, Tl / pt, Hl / ph, Wl / pw].  Four consecutive elements
 // of a row per thread (Wl % 4 == 0, 16-byte aligned tensors: 16-byte loads
 // and stores).  z_out may be z_target or z_hist: each element is read before
-// it is written, by the same thread.
+// it is written, by the same thread.  I is the index type: 32-bit whenever
+// the latent has fewer than 2^32 elements (the row and column of a quad take
+// a few divisions, which 64-bit integers make several times dearer).
+template <typename I>
 __global__ void __launch_bounds__(256) fusion4_kernel(const float4 *zt, const float4 *zh,
                                                       const float *__restrict__ weight,
-                                                      float4 *zo, int64_t quads, int C, int Tl,
-                                                      int Hl, int Wl, int pt, int ph, int pw) {
-  const int64_t qi = (int64_t)blockIdx.x * 256 + threadIdx.x;
+                                                      float4 *zo, I quads, I C, I Tl, I Hl, I Wl,
+                                                      I pt, I ph, I pw) {
+  const I qi = (I)blockIdx.x * 256 + threadIdx.x;
   if (qi >= quads) return;
-  const int64_t e = qi * 4;
-  const int x0 = (int)(e % Wl);
-  int64_t r = e / Wl;
-  const int y = (int)(r % Hl);
-  r /= Hl;
-  const int tt = (int)(r % Tl);
-  const int b = (int)(r / Tl / C);
-  const int Tg = Tl / pt, Hg = Hl / ph, Wg = Wl / pw;
-  const float *wrow = weight + (((int64_t)b * Tg + tt / pt) * Hg + y / ph) * Wg;
+  const I e = qi * 4;
+  const I row = e / Wl;  // (b, c, t, y)
+  const I x0 = e - row * Wl;
+  const I bct = row / Hl;
+  const I y = row - bct * Hl;
+  const I bc = bct / Tl;
+  const I tt = bct - bc * Tl;
+  const I b = bc / C;
+  const I Tg = Tl / pt, Hg = Hl / ph, Wg = Wl / pw;
+  const float *wrow = weight + ((size_t)(b * Tg + tt / pt) * Hg + y / ph) * Wg;
   const float4 a = zt[qi], h = zh[qi];
-  const float w0 = wrow[x0 / pw], w1 = wrow[(x0 + 1) / pw], w2 = wrow[(x0 + 2) / pw],
-              w3 = wrow[(x0 + 3) / pw];
+  float w0, w1, w2, w3;
+  if (pw == 1) {
+    w0 = wrow[x0], w1 = wrow[x0 + 1], w2 = wrow[x0 + 2], w3 = wrow[x0 + 3];
+  } else {
+    w0 = wrow[x0 / pw], w1 = wrow[(x0 + 1) / pw], w2 = wrow[(x0 + 2) / pw], w3 = wrow[(x0 + 3) / pw];
+  }
   float4 o;
   o.x = w0 * a.x + (1.f - w0) * h.x;
   o.y = w1 * a.y + (1.f - w1) * h.y;
@@ -211,9 +220,18 @@ hipError_t launch_fusion(const float *zt, const float *zh, const float *weight, 
                                     reinterpret_cast<uintptr_t>(zo)) % 16) == 0;
   if (vec) {
     const int64_t quads = total / 4;
-    hipLaunchKernelGGL(fusion4_kernel, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, s,
-                       reinterpret_cast<const float4 *>(zt), reinterpret_cast<const float4 *>(zh),
-                       weight, reinterpret_cast<float4 *>(zo), quads, C, Tl, Hl, Wl, pt, ph, pw);
+    const dim3 grid((unsigned)((quads + 255) / 256));
+    auto f4 = reinterpret_cast<const float4 *>(zt);
+    auto h4 = reinterpret_cast<const float4 *>(zh);
+    auto o4 = reinterpret_cast<float4 *>(zo);
+    if (total < ((int64_t)1 << 32))
+      hipLaunchKernelGGL(fusion4_kernel<uint32_t>, grid, dim3(256), 0, s, f4, h4, weight, o4,
+                         (uint32_t)quads, (uint32_t)C, (uint32_t)Tl, (uint32_t)Hl, (uint32_t)Wl,
+                         (uint32_t)pt, (uint32_t)ph, (uint32_t)pw);
+    else
+      hipLaunchKernelGGL(fusion4_kernel<uint64_t>, grid, dim3(256), 0, s, f4, h4, weight, o4,
+                         (uint64_t)quads, (uint64_t)C, (uint64_t)Tl, (uint64_t)Hl, (uint64_t)Wl,
+                         (uint64_t)pt, (uint64_t)ph, (uint64_t)pw);
   } else {
     hipLaunchKernelGGL(fusion1_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, zt,
                        zh, weight, zo, total, C, Tl, Hl, Wl, pt, ph, pw);
