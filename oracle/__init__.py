@@ -25,6 +25,9 @@ Every function is plain fp64 NumPy, written from the paper's definitions:
   ``compact_restricted``: the region-restricted middle-layer path (Sec. 3.3
   "Region-Guided Latent Reuse" and "Joint Reuse in Intermediate Layers";
   Appendix C.3 radii).
+* ``exact_block_mass`` / ``select_row_mass`` / ``mask_from_mass``: the
+  token-level attention mass of each block pair and the selection on it
+  (Appendix C.3, "source attention mass" read literally).
 * ``block_sparse_attention``: softmax attention of the recomputed target
   Q, K, V restricted to the reused block structure (Sec. 3.3, "Historical
   Sparse-Connectivity Reuse"; Appendix C.3).
@@ -39,6 +42,7 @@ from .mask import (pool_blocks, block_scores, select_row, build_block_mask,
                    merge_target_rows, compact_mask, row_admissible_masks, TIE_EPS,
                    FRAGILE_EPS, pack_mask, unpack_mask)
 from .attention import block_sparse_attention, token_mask_from_blocks
+from .exact_mass import exact_block_mass, select_row_mass, mask_from_mass
 from .region import (dilate_frames, chebyshev_distance, smoothstep, regions, latent_fusion,
                      region_block_flags, restrict_mask, compact_restricted)
 from .cosine import cosine_similarity, topk_cosine
@@ -51,4 +55,5 @@ __all__ = [
     "cosine_similarity", "topk_cosine", "to_f64",
     "dilate_frames", "chebyshev_distance", "smoothstep", "regions", "latent_fusion",
     "region_block_flags", "restrict_mask", "compact_restricted",
+    "exact_block_mass", "select_row_mass", "mask_from_mass",
 ]
