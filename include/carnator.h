@@ -6,6 +6,10 @@
  * with Generation-Native Compatibility-Guided Cross-Request Reuse":
  *
  *   carnator_build_block_mask   historical block connectivity (Appendix C.3)
+ *   carnator_block_mass_exact, carnator_select_block_mask
+ *                               the builder on the exact token-level
+ *                               attention mass of each block pair
+ *                               (Appendix C.3, "source attention mass")
  *   carnator_merge_target_rows  target-specific query blocks widened to full
  *                               rows (Sec. 3.3, joint reuse in the middle
  *                               layers)
@@ -74,7 +78,7 @@
 extern "C" {
 #endif
 
-#define CARNATOR_ABI_VERSION 3
+#define CARNATOR_ABI_VERSION 4
 
 typedef enum {
   CARNATOR_OK = 0,
@@ -173,6 +177,47 @@ size_t carnator_compact_block_mask_workspace_size(const carnator_shape *shape);
 int carnator_compact_block_mask(const uint8_t *mask, const carnator_shape *shape,
                                 int32_t *row_ptr, int32_t *col_idx, int32_t *order,
                                 void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Exact block mass -- Appendix C.3 keeps, per head and query block, the
+ * smallest set of key blocks covering a fixed fraction of the source
+ * attention mass.  carnator_build_block_mask estimates that mass from block
+ * means; these calls compute it from the tokens:
+ *
+ *   M[b,h,i,j] = (1 / n_i) sum_{a in block i, a < N} sum_{t in block j}
+ *                softmax_t(sigma q_a . k_t)
+ *
+ * the softmax over all N keys, sigma = scale or 1/sqrt(head_dim) when
+ * scale <= 0; n_i the valid queries of block i; each row sums to 1.  A dense
+ * bf16 matrix-core pass (fp32 accumulation and softmax statistics), the
+ * masses formed in fp64.
+ *
+ * carnator_block_mass_exact:
+ *   q_hist, k_hist  bf16 views [B, H, N, d]
+ *   mass            fp64 [B, H, nB, nB] out
+ *   workspace       carnator_block_mass_exact_workspace_size(shape) bytes,
+ *                   256-byte aligned (8 B per (query, key block) plus 4 B
+ *                   per query: 0.8 GB at B=1, H=12, N=32,760, block 128)
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_WORKSPACE, E_HIP.
+ *
+ * carnator_select_block_mask: the selection of carnator_build_block_mask
+ * applied to given masses: per row, the smallest prefix of the key blocks
+ * by descending mass (lower index first on equal mass) whose mass reaches
+ * mass_threshold of the row total; masses within 1e-6 of the cut mass are
+ * tied and the lower block indices among them are kept; mass_threshold
+ * >= 1 keeps every block.
+ *   mass      fp64 [B, H, nB, nB] (non-negative)
+ *   mask_out  uint8 [B, H, nB, nB] or NULL; bits_out uint64 [B, H, nB, W]
+ *             or NULL: exactly one of them
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_HIP.
+ */
+size_t carnator_block_mass_exact_workspace_size(const carnator_shape *shape);
+int carnator_block_mass_exact(const carnator_view *q_hist, const carnator_view *k_hist,
+                              const carnator_shape *shape, float scale, double *mass,
+                              void *workspace, size_t workspace_bytes, hipStream_t stream);
+int carnator_select_block_mask(const double *mass, const carnator_shape *shape,
+                               double mass_threshold, uint8_t *mask_out, uint64_t *bits_out,
+                               hipStream_t stream);
 
 /*
  * Bit-packed masks: the historical block connectivity in its stored form.

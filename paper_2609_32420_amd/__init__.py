@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libcarnator.so")
 
 CARNATOR_OK = 0
 # CARNATOR_ABI_VERSION of include/carnator.h this binding marshals for
-ABI_VERSION = 3
+ABI_VERSION = 4
 STATUS = {0: "OK", -1: "E_NULL", -2: "E_SHAPE", -3: "E_UNSUPPORTED", -4: "E_ALIGN",
           -5: "E_WORKSPACE", -6: "E_HIP"}
 
@@ -28,6 +28,7 @@ EXPORTS = (
     "carnator_abi_version", "carnator_status_str", "carnator_last_error",
     "carnator_build_block_mask_workspace_size", "carnator_build_block_mask",
     "carnator_merge_target_rows",
+    "carnator_block_mass_exact_workspace_size", "carnator_block_mass_exact", "carnator_select_block_mask",
     "carnator_compact_block_mask_workspace_size", "carnator_compact_block_mask",
     "carnator_build_block_mask_bits", "carnator_pack_block_mask", "carnator_unpack_block_mask",
     "carnator_compact_block_mask_bits_workspace_size", "carnator_compact_block_mask_bits",
@@ -76,6 +77,9 @@ def lib() -> ctypes.CDLL:
             "carnator_build_block_mask_workspace_size": (SZ, [SP]),
             "carnator_build_block_mask": (ctypes.c_int, [VP, VP, SP, F32, F64, P, P, SZ, P]),
             "carnator_merge_target_rows": (ctypes.c_int, [P, SP, P, P, P]),
+            "carnator_block_mass_exact_workspace_size": (SZ, [SP]),
+            "carnator_block_mass_exact": (ctypes.c_int, [VP, VP, SP, F32, P, P, SZ, P]),
+            "carnator_select_block_mask": (ctypes.c_int, [P, SP, F64, P, P, P]),
             "carnator_compact_block_mask_workspace_size": (SZ, [SP]),
             "carnator_compact_block_mask": (ctypes.c_int, [P, SP, P, P, P, P, SZ, P]),
             "carnator_build_block_mask_bits": (ctypes.c_int, [VP, VP, SP, F32, F64, P, P, SZ, P]),
@@ -175,6 +179,44 @@ def build_block_mask(q_hist: torch.Tensor, k_hist: torch.Tensor, block: int, mas
     _check(L.carnator_build_block_mask(ctypes.byref(qv), ctypes.byref(kv), ctypes.byref(s), float(scale),
                                        float(mass_threshold), _ptr(out), _ptr(ws), ws.numel(),
                                        _stream(q_hist)))
+    return out
+
+
+def block_mass_exact(q_hist: torch.Tensor, k_hist: torch.Tensor, block: int, scale: float = 0.0,
+                     out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Token-level attention mass of every block pair, fp64 [B, H, nB, nB]
+    (carnator_block_mass_exact)."""
+    s = _shape(q_hist, block)
+    if tuple(k_hist.shape) != tuple(q_hist.shape):
+        raise ValueError("q_hist and k_hist shapes differ")
+    nb = -(-s.seq_len // block)
+    if out is None:
+        out = torch.empty(s.batch, s.heads, nb, nb, dtype=torch.float64, device=q_hist.device)
+    if out.dtype != torch.float64 or not out.is_contiguous() or tuple(out.shape) != (s.batch, s.heads, nb, nb):
+        raise ValueError("out must be a contiguous fp64 [B, H, nB, nB] tensor")
+    L = lib()
+    if workspace is None:
+        workspace = _workspace(L.carnator_block_mass_exact_workspace_size(ctypes.byref(s)), q_hist.device)
+    qv, kv = _view(q_hist), _view(k_hist)
+    _check(L.carnator_block_mass_exact(ctypes.byref(qv), ctypes.byref(kv), ctypes.byref(s), float(scale), _ptr(out),
+                                       _ptr(workspace), workspace.numel(), _stream(q_hist)))
+    return out
+
+
+def select_block_mask(mass: torch.Tensor, mass_threshold: float, bits: bool = False,
+                      out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Top-mass selection on given masses fp64 [B, H, nB, nB]: uint8 mask, or
+    the packed int64 [B, H, nB, W] with bits=True (carnator_select_block_mask)."""
+    if mass.dim() != 4 or mass.dtype != torch.float64 or not mass.is_contiguous():
+        raise ValueError("mass must be a contiguous fp64 [B, H, nB, nB] tensor")
+    B, H, nb, _ = mass.shape
+    if out is None:
+        out = (torch.empty(B, H, nb, mask_words(nb), dtype=torch.int64, device=mass.device) if bits
+               else torch.empty(B, H, nb, nb, dtype=torch.uint8, device=mass.device))
+    s = Shape(B, H, nb * 64, 64, 64)
+    _check(lib().carnator_select_block_mask(_ptr(mass), ctypes.byref(s), float(mass_threshold),
+                                            None if bits else _ptr(out), _ptr(out) if bits else None,
+                                            _stream(mass)))
     return out
 
 

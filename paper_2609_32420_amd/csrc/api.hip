@@ -190,6 +190,55 @@ int carnator_build_block_mask_bits(const carnator_view *q_hist, const carnator_v
                     ws_bytes, stream);
 }
 
+// ---------------------------------------------------------------- exact block mass
+
+size_t carnator_block_mass_exact_workspace_size(const carnator_shape *s) {
+  if (check_shape(s) != CARNATOR_OK) return 0;
+  return mass_scratch_bytes(s->batch * s->heads, s->seq_len, n_blocks(s));
+}
+
+int carnator_block_mass_exact(const carnator_view *q_hist, const carnator_view *k_hist,
+                              const carnator_shape *s, float scale, double *mass, void *workspace,
+                              size_t ws_bytes, hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if ((rc = check_view(q_hist, s, "q_hist"))) return rc;
+  if ((rc = check_view(k_hist, s, "k_hist"))) return rc;
+  if (!mass) return fail(CARNATOR_E_NULL, "mass is NULL");
+  if (reinterpret_cast<uintptr_t>(mass) % 8 != 0)
+    return fail(CARNATOR_E_ALIGN, "mass must be 8-byte aligned");
+  if (!isfinite(scale)) return fail(CARNATOR_E_SHAPE, "scale must be finite");
+  if ((rc = check_ws(workspace, ws_bytes, carnator_block_mass_exact_workspace_size(s)))) return rc;
+  const float sc = scale > 0.f ? scale : (float)(1.0 / sqrt((double)s->head_dim));
+  hipError_t e = launch_mass(to_view(q_hist), to_view(k_hist), s->batch, s->heads, s->seq_len,
+                             s->head_dim, s->block, sc, mass, workspace, stream);
+  if (e != hipSuccess) return hip_fail(e, "mass");
+  return ok();
+}
+
+int carnator_select_block_mask(const double *mass, const carnator_shape *s, double mass_threshold,
+                               uint8_t *mask_out, uint64_t *bits_out, hipStream_t stream) {
+  int rc;
+  if ((rc = check_shape(s))) return rc;
+  if (!mass) return fail(CARNATOR_E_NULL, "mass is NULL");
+  if ((mask_out == nullptr) == (bits_out == nullptr))
+    return fail(CARNATOR_E_NULL, "exactly one of mask_out and bits_out must be non-NULL");
+  if (reinterpret_cast<uintptr_t>(mass) % 8 != 0 ||
+      (bits_out && reinterpret_cast<uintptr_t>(bits_out) % 8 != 0))
+    return fail(CARNATOR_E_ALIGN, "mass and bits_out must be 8-byte aligned");
+  if (!(mass_threshold > 0.0)) return fail(CARNATOR_E_SHAPE, "mass_threshold must be > 0");
+  const int nB = n_blocks(s);
+  const int BH = s->batch * s->heads;
+  hipError_t e;
+  if (mass_threshold >= 1.0)
+    e = bits_out ? launch_fill_ones_bits(bits_out, (int64_t)BH * nB, nB, stream)
+                 : launch_fill_ones(mask_out, (size_t)BH * nB * nB, stream);
+  else
+    e = launch_select_mass(mass, BH, nB, mass_threshold, mask_out, bits_out, stream);
+  if (e != hipSuccess) return hip_fail(e, "select_mass");
+  return ok();
+}
+
 // ---------------------------------------------------------------- merge
 
 int carnator_merge_target_rows(uint8_t *mask, const carnator_shape *s, const uint8_t *target_rows,

@@ -92,6 +92,17 @@ hipError_t launch_pool(View q, View k, int B, int H, int N, int d, int bs, doubl
 hipError_t launch_select(const double *qbar, const double *kbar, int BH, int nB, int d,
                          double sigma, double tau, uint8_t *mask, uint64_t *bits, hipStream_t s);
 hipError_t launch_fill_ones(uint8_t *p, size_t n, hipStream_t s);
+// The same selection on given block masses [BH][nB][nB] (no softmax).
+hipError_t launch_select_mass(const double *mass, int BH, int nB, double tau, uint8_t *mask,
+                              uint64_t *bits, hipStream_t s);
+
+// ---- exact block mass ----------------------------------------------------------
+// M[bh][i][j] = mean over the valid queries of block i of the softmax mass of
+// key block j (fp64, rows sum to 1), by a dense bf16 MFMA pass over the
+// historical Q and K; scratch of mass_scratch_bytes.
+size_t mass_scratch_bytes(int BH, int N, int nB);
+hipError_t launch_mass(View q, View k, int B, int H, int N, int d, int bs, float scale,
+                       double *mass, void *scratch, hipStream_t s);
 
 // ---- merge -----------------------------------------------------------------
 hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows,

@@ -112,7 +112,10 @@ __device__ inline double key_value(uint64_t k) {
 // its channels in the same order.  With R = 8 the upper half of the tile
 // repeats row R - 1 and is not stored.  Phase 2: wave w selects rows w,
 // w + W, ... of the workgroup (E = positions per lane, 64 E >= nB).
-template <int D, int E, int R, int W>
+// MASS: the rows are given, as block masses [BH][nB][nB] at qbar (kbar and
+// sigma unused): phase 1 copies the workgroup's rows into LDS and phase 2
+// selects on the masses themselves instead of the softmax of logits.
+template <int D, int E, int R, int W, bool MASS>
 __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict__ qbar,
                                                         const double *__restrict__ kbar, int nB,
                                                         double sigma, double tau,
@@ -139,63 +142,69 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
 
-  double *qs = sc + R * nB;
-  {
-    constexpr int SPT = R * D / (64 * W);  // staged values per thread (all loads in flight)
-    double sv[SPT];
-#pragma unroll
-    for (int i = 0; i < SPT; ++i) {
-      const int x = threadIdx.x + i * 64 * W, r = x / D, c = x - r * D;
-      sv[i] = qb[min(r, nr - 1) * D + c];
-    }
-#pragma unroll
-    for (int i = 0; i < SPT; ++i) {
-      const int x = threadIdx.x + i * 64 * W, r = x / D, c = x - r * D;
-      qs[r * QS + c] = sv[i];
-    }
-  }
-  __syncthreads();
-  {
-    typedef double f64x4 __attribute__((ext_vector_type(4)));
-    constexpr int NG = D / 16;  // 16-channel groups
-    const int li = lane & 15, lk = lane >> 4;
-    const double *qr = qs + min(li, R - 1) * QS + 4 * lk;
-    // The groups start at a different place in every wave: walking them in
-    // lockstep sends every wave of the chip to the same few L2 channels.
-    const int rot = (wave * 5 + T * 3) & (NG - 1);
-    for (int j0 = wave * 16; j0 < nB; j0 += 16 * W) {
-      const double *kr = kb + (int64_t)min(j0 + li, nB - 1) * D + 4 * lk;
-      f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-      // All of the tile's loads are issued before the first product: left to
-      // itself the compiler keeps two in flight, and the tile then costs
-      // D / 8 L2 round trips instead of one.
-      double2 kv[NG][2];
-#pragma unroll
-      for (int g = 0; g < NG; ++g) {
-        const int gr = (g + rot) & (NG - 1);
-        kv[g][0] = *reinterpret_cast<const double2 *>(kr + 16 * gr);
-        kv[g][1] = *reinterpret_cast<const double2 *>(kr + 16 * gr + 2);
+  if constexpr (MASS) {
+    const double *src = qbar + ((int64_t)bh * nB + r0) * nB;
+    for (int x = threadIdx.x; x < nr * nB; x += 64 * W) sc[x] = src[x];
+    __syncthreads();
+  } else {
+    double *qs = sc + R * nB;
+    {
+      constexpr int SPT = R * D / (64 * W);  // staged values per thread (all loads in flight)
+      double sv[SPT];
+  #pragma unroll
+      for (int i = 0; i < SPT; ++i) {
+        const int x = threadIdx.x + i * 64 * W, r = x / D, c = x - r * D;
+        sv[i] = qb[min(r, nr - 1) * D + c];
       }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int g = 0; g < NG; ++g) {
-        const int gr = (g + rot) & (NG - 1);
-        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 0], kv[g][0].x, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 1], kv[g][0].y, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 2], kv[g][1].x, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 3], kv[g][1].y, acc, 0, 0, 0);
+  #pragma unroll
+      for (int i = 0; i < SPT; ++i) {
+        const int x = threadIdx.x + i * 64 * W, r = x / D, c = x - r * D;
+        qs[r * QS + c] = sv[i];
       }
-      const int j = j0 + li;
-      if (j < nB) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int r = lk + 4 * v;
-          if (r < nr) sc[r * nB + j] = sigma * acc[v];
+    }
+    __syncthreads();
+    {
+      typedef double f64x4 __attribute__((ext_vector_type(4)));
+      constexpr int NG = D / 16;  // 16-channel groups
+      const int li = lane & 15, lk = lane >> 4;
+      const double *qr = qs + min(li, R - 1) * QS + 4 * lk;
+      // The groups start at a different place in every wave: walking them in
+      // lockstep sends every wave of the chip to the same few L2 channels.
+      const int rot = (wave * 5 + T * 3) & (NG - 1);
+      for (int j0 = wave * 16; j0 < nB; j0 += 16 * W) {
+        const double *kr = kb + (int64_t)min(j0 + li, nB - 1) * D + 4 * lk;
+        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+        // All of the tile's loads are issued before the first product: left to
+        // itself the compiler keeps two in flight, and the tile then costs
+        // D / 8 L2 round trips instead of one.
+        double2 kv[NG][2];
+  #pragma unroll
+        for (int g = 0; g < NG; ++g) {
+          const int gr = (g + rot) & (NG - 1);
+          kv[g][0] = *reinterpret_cast<const double2 *>(kr + 16 * gr);
+          kv[g][1] = *reinterpret_cast<const double2 *>(kr + 16 * gr + 2);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+  #pragma unroll
+        for (int g = 0; g < NG; ++g) {
+          const int gr = (g + rot) & (NG - 1);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 0], kv[g][0].x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 1], kv[g][0].y, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 2], kv[g][1].x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qr[16 * gr + 3], kv[g][1].y, acc, 0, 0, 0);
+        }
+        const int j = j0 + li;
+        if (j < nB) {
+  #pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int r = lk + 4 * v;
+            if (r < nr) sc[r * nB + j] = sigma * acc[v];
+          }
         }
       }
     }
+    __syncthreads();
   }
-  __syncthreads();
 
   // ---- phase 2: selection, one row per wave.  Lane l holds positions
   // u 64 + l.  The k-th largest selection key K* (k the shortest prefix whose
@@ -227,7 +236,8 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
     double lsum = 0.0;
 #pragma unroll
     for (int u = 0; u < E; ++u) {
-      pl[u] = (u * 64 + lane < nB) ? exp(pl[u] - smax) : 0.0;
+      if constexpr (MASS) pl[u] = (u * 64 + lane < nB) ? pl[u] : 0.0;
+      else pl[u] = (u * 64 + lane < nB) ? exp(pl[u] - smax) : 0.0;
       lsum += pl[u];
     }
     const double tauZ = tau * wave_sum(lsum);
@@ -364,7 +374,7 @@ hipError_t launch_pool(View q, View k, int B, int H, int N, int d, int bs, doubl
   return hipGetLastError();
 }
 
-template <int D, int R, int W>
+template <int D, int R, int W, bool MASS>
 static hipError_t launch_select_dr(const double *qbar, const double *kbar, int BH, int nB,
                                    double sigma, double tau, uint8_t *mask, uint64_t *bits,
                                    hipStream_t s) {
@@ -374,10 +384,10 @@ static hipError_t launch_select_dr(const double *qbar, const double *kbar, int B
   const int need = (nB + 63) / 64;  // positions per lane
 #define CARNATOR_SEL(EE)                                                                          \
   do {                                                                                            \
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&select_kernel<D, EE, R, W>), \
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&select_kernel<D, EE, R, W, MASS>), \
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);     \
     if (e != hipSuccess) return e;                                                                \
-    hipLaunchKernelGGL((select_kernel<D, EE, R, W>), grid, dim3(64 * W), lds, s, qbar, kbar, nB, \
+    hipLaunchKernelGGL((select_kernel<D, EE, R, W, MASS>), grid, dim3(64 * W), lds, s, qbar, kbar, nB, \
                        sigma, tau, mask, bits, BH);                                               \
   } while (0)
   // W = 16 waves (1024 threads, at most 128 VGPRs) only while a lane holds at
@@ -416,9 +426,9 @@ template <int D>
 static hipError_t launch_select_d(const double *qbar, const double *kbar, int BH, int nB,
                                   double sigma, double tau, uint8_t *mask, uint64_t *bits,
                                   hipStream_t s) {
-  if (nB <= 512) return launch_select_dr<D, 16, 16>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
-  if (nB <= 1024) return launch_select_dr<D, 16, 8>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
-  return launch_select_dr<D, 8, 8>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
+  if (nB <= 512) return launch_select_dr<D, 16, 16, false>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
+  if (nB <= 1024) return launch_select_dr<D, 16, 8, false>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
+  return launch_select_dr<D, 8, 8, false>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
 }
 
 hipError_t launch_select(const double *qbar, const double *kbar, int BH, int nB, int d,
@@ -426,6 +436,14 @@ hipError_t launch_select(const double *qbar, const double *kbar, int BH, int nB,
                          hipStream_t s) {
   if (d == 128) return launch_select_d<128>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
   return launch_select_d<64>(qbar, kbar, BH, nB, sigma, tau, mask, bits, s);
+}
+
+hipError_t launch_select_mass(const double *mass, int BH, int nB, double tau, uint8_t *mask,
+                              uint64_t *bits, hipStream_t s) {
+  // the pooled-row area of the LDS layout is not used: the smallest D
+  if (nB <= 512) return launch_select_dr<64, 16, 16, true>(mass, nullptr, BH, nB, 1.0, tau, mask, bits, s);
+  if (nB <= 1024) return launch_select_dr<64, 16, 8, true>(mass, nullptr, BH, nB, 1.0, tau, mask, bits, s);
+  return launch_select_dr<64, 8, 8, true>(mass, nullptr, BH, nB, 1.0, tau, mask, bits, s);
 }
 
 hipError_t launch_fill_ones(uint8_t *p, size_t n, hipStream_t s) {

@@ -241,3 +241,25 @@ def test_region_entry_points_reject(L):
     ar = L.carnator_block_sparse_attn_rows
     assert ar(ctypes.byref(q), ctypes.byref(q), ctypes.byref(q), ctypes.c_void_p(0x20000), 0, 0, 64,
               ctypes.byref(_shape()), p, p, p, None, 0.0, None, None) == -1
+
+
+def test_exact_mass_entry_points_reject(L):
+    s = _shape()
+    q = _view()
+    p = ctypes.c_void_p(0x20000)
+    ws = ctypes.c_void_p(0x40000)
+    m = L.carnator_block_mass_exact
+    assert m(ctypes.byref(q), ctypes.byref(q), ctypes.byref(s), 0.0, None, ws, 1 << 30, None) == -1
+    assert m(ctypes.byref(q), ctypes.byref(q), ctypes.byref(s), 0.0, ctypes.c_void_p(0x20004), ws, 1 << 30,
+             None) == -4
+    assert m(ctypes.byref(q), ctypes.byref(q), ctypes.byref(s), 0.0, p, ws, 16, None) == -5
+    assert m(ctypes.byref(q), ctypes.byref(q), ctypes.byref(s), float("inf"), p, ws, 1 << 30, None) == -2
+    # one 8-byte record per (query, key block) and a 4-byte log-sum-exp per query
+    big = _shape(1, 12, 32760, 128, 128)
+    assert L.carnator_block_mass_exact_workspace_size(ctypes.byref(big)) >= 12 * 32760 * (256 * 8 + 4)
+    sel = L.carnator_select_block_mask
+    assert sel(None, ctypes.byref(s), 0.9, p, None, None) == -1
+    assert sel(p, ctypes.byref(s), 0.9, None, None, None) == -1
+    assert sel(p, ctypes.byref(s), 0.9, p, p, None) == -1
+    assert sel(p, ctypes.byref(s), 0.0, p, None, None) == -2
+    assert sel(ctypes.c_void_p(0x20004), ctypes.byref(s), 0.9, p, None, None) == -4

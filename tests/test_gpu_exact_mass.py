@@ -1,0 +1,108 @@
+"""Parity of the exact-mass builder (through the C ABI) with the oracle.
+
+Block masses: |dM| <= 1e-4 M + 1e-7 against the fp64 oracle (bf16 inputs,
+fp32 scores and softmax statistics: about 1e-6 relative per score, 1e-5
+after the exponent), rows summing to 1 within 1e-5.  Selection on given
+masses: bit-exact against the oracle's selection on the same fp64 masses,
+except rows whose decision lies within 1e-9 of a threshold (reported).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_32420_amd as P
+import synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _rand(B, H, N, d, seed, scale):
+    g = torch.Generator().manual_seed(seed)
+    q = (torch.randn(B, H, N, d, generator=g) * scale).to(torch.bfloat16)
+    k = (torch.randn(B, H, N, d, generator=g) * scale).to(torch.bfloat16)
+    return q.to(DEV), k.to(DEV)
+
+
+def _check_mass(got, want):
+    g = got.cpu().numpy()
+    ok = ~np.isnan(want)
+    err = np.abs(g[ok] - want[ok])
+    assert (err <= 1e-4 * want[ok] + 1e-7).all(), float((err / (want[ok] + 1e-7)).max())
+    return g
+
+
+@pytest.mark.parametrize("N,bs,d,scale", [(50, 64, 64, 1.0), (64, 64, 128, 0.6), (200, 64, 128, 1.0),
+                                          (333, 128, 64, 1.5), (1000, 128, 128, 1.0), (257, 128, 128, 3.0)])
+def test_block_mass_random_shapes(N, bs, d, scale):
+    q, k = _rand(2, 2, N, d, N + d, scale)
+    _say("mass", N, bs, d, scale)
+    got = P.block_mass_exact(q, k, bs)
+    want = oracle.exact_block_mass(oracle.to_f64(q), oracle.to_f64(k), bs)
+    g = _check_mass(got, want)
+    np.testing.assert_allclose(g.sum(axis=-1), 1.0, atol=1e-5)
+
+
+def test_block_mass_explicit_scale_and_strided_views():
+    # [B, N, H, d] storage viewed as [B, H, N, d]
+    g = torch.Generator().manual_seed(3)
+    base = (torch.randn(1, 300, 3, 64, generator=g)).to(torch.bfloat16).to(DEV)
+    kb = (torch.randn(1, 300, 3, 64, generator=g)).to(torch.bfloat16).to(DEV)
+    q, k = base.permute(0, 2, 1, 3), kb.permute(0, 2, 1, 3)
+    got = P.block_mass_exact(q, k, 64, scale=0.3)
+    want = oracle.exact_block_mass(oracle.to_f64(q), oracle.to_f64(k), 64, scale=0.3)
+    _check_mass(got, want)
+
+
+@pytest.mark.parametrize("wid", [0, 1, 2])
+def test_block_mass_workloads(wid):
+    wl = synth.WORKLOADS[wid]
+    heads = None if wid == 0 else 2
+    x = synth.attention_inputs(wl, seed=0, device=DEV, heads=heads)
+    _say("mass workload", wl.name, "heads", heads)
+    got = P.block_mass_exact(x["q_hist"], x["k_hist"], wl.block)
+    nb = wl.n_blocks
+    rng = np.random.default_rng(wid)
+    H = x["q_hist"].shape[1]
+    rows = sorted({(0, int(rng.integers(0, H)), int(rng.integers(0, nb))) for _ in range(6)} |
+                  {(0, H - 1, nb - 1), (0, 0, 0)})
+    want = oracle.exact_block_mass(oracle.to_f64(x["q_hist"]), oracle.to_f64(x["k_hist"]), wl.block, rows=rows)
+    g = _check_mass(got, want)
+    np.testing.assert_allclose(g.sum(axis=-1), 1.0, atol=1e-5)
+
+
+@pytest.mark.parametrize("wid", [1, 3])
+def test_selection_on_masses_bit_exact(wid):
+    wl = synth.WORKLOADS[wid]
+    x = synth.attention_inputs(wl, seed=1, device=DEV, heads=2)
+    mass = P.block_mass_exact(x["q_hist"], x["k_hist"], wl.block)
+    m = mass.cpu().numpy()
+    want, rep = oracle.mask_from_mass(m, wl.tau)
+    got = P.select_block_mask(mass, wl.tau).cpu().numpy()
+    bad = [tuple(r) for r in np.argwhere((got != want).any(axis=-1))]
+    assert set(bad) <= set(rep["fragile"]), bad[:5]
+    bits = P.select_block_mask(mass, wl.tau, bits=True)
+    np.testing.assert_array_equal(bits.cpu().numpy().view(np.uint64), oracle.pack_mask(got))
+    pooled = P.build_block_mask(x["q_hist"], x["k_hist"], wl.block, wl.tau).cpu().numpy()
+    inter = (pooled & got).sum()
+    _say("exact vs pooled: density %.4f vs %.4f, jaccard %.3f, fragile %d" % (
+        got.mean(), pooled.mean(), inter / max((pooled | got).sum(), 1), len(rep["fragile"])))
+
+
+@pytest.mark.parametrize("nb,tau", [(10, 0.45), (300, 0.123), (129, 1.0)])
+def test_selection_on_equal_masses(nb, tau):
+    # every mass equal: k = ceil(tau nB), the lowest blocks (tau = 1: all)
+    mass = torch.full((1, 2, nb, nb), 1.0 / nb, dtype=torch.float64, device=DEV)
+    got = P.select_block_mask(mass, tau).cpu().numpy()
+    k = nb if tau >= 1 else int(np.ceil(tau * nb))
+    want = np.zeros(nb, np.uint8)
+    want[:k] = 1
+    assert (got == want).all()
