@@ -28,6 +28,11 @@ region, the latent blend (HBM-bound; its GB/s against the 8 TB/s peak),
 block flags, compaction restricted to active rows and context keys, and
 the attention of the active rows only -- each timed alone.
 
+``exact_mass`` (after the timed region, skipped with --no-exact): the
+builder on the token-level attention mass -- the dense mass pass against
+the bf16 MFMA peak and the selection on its masses -- with the exact masks
+compared to the pooled ones.
+
 ``mask_bank`` (after the timed region, skipped with --no-bank): the same
 masks in their stored, bit-packed form -- the builder writing a bank slot
 directly, compaction of a slot with the widening applied while reading, and
@@ -172,6 +177,62 @@ def bank_pass(P, torch, stream, sets, flags, masks, lists, ws_mask, wl, steps):
 LATENT_CHANNELS, LATENT_PATCH = 16, (1, 2, 2)
 
 
+def exact_mass_pass(P, torch, stream, sets, wl, steps):
+    """The exact-mass builder on the same historical Q/K, after the timed
+    region: token-level block masses (one dense bf16 QK^T pass and the
+    reduction) and the selection on them, each call timed alone; the mass
+    pass against the bf16 MFMA peak (dense QK^T FLOPs 2 d N^2 per head); the
+    exact masks compared with the pooled ones of the same sets (before
+    widening)."""
+    B, H, N, d, bs, nb = wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block, wl.n_blocks
+    dev = sets[0][0]["q"].device
+    mass = torch.empty(B, H, nb, nb, dtype=torch.float64, device=dev)
+    ws = torch.empty(P.lib().carnator_block_mass_exact_workspace_size(ctypes_shape(P, wl)), dtype=torch.uint8,
+                     device=dev)
+    mask = torch.empty(B, H, nb, nb, dtype=torch.uint8, device=dev)
+    t_mass, t_sel = [], []
+    agree = []
+    for i in range(steps + 1):
+        si = i % len(sets)
+        x = sets[si][0]
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(stream)
+        P.block_mass_exact(x["q_hist"], x["k_hist"], bs, out=mass, workspace=ws)
+        e[1].record(stream)
+        P.select_block_mask(mass, wl.tau, out=mask)
+        e[2].record(stream)
+        if i == 0:
+            continue
+        t_mass.append((e[0], e[1]))
+        t_sel.append((e[1], e[2]))
+        if i <= len(sets):
+            pooled = P.build_block_mask(x["q_hist"], x["k_hist"], bs, wl.tau)
+            inter = int((pooled & mask).sum().item())
+            union = int((pooled | mask).sum().item())
+            agree.append((float(mask.float().mean().item()), float(pooled.float().mean().item()),
+                          inter / max(union, 1)))
+    torch.cuda.synchronize()
+    ms_mass = float(np.mean([a.elapsed_time(b) for a, b in t_mass]))
+    ms_sel = float(np.mean([a.elapsed_time(b) for a, b in t_sel]))
+    flops = 2.0 * d * float(N) * float(N) * B * H
+    return {
+        "mass_ms_per_call": round(ms_mass, 4),
+        "mass_qk_tflop": round(flops / 1e12, 4),
+        "mass_tflops": round(flops / (ms_mass * 1e-3) / 1e12, 2),
+        "mass_pct_bf16_peak": round(100.0 * flops / (ms_mass * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2),
+        "select_ms_per_call": round(ms_sel, 4),
+        "workspace_GB": round(ws.numel() / 1e9, 3),
+        "density_exact": [round(a[0], 4) for a in agree],
+        "density_pooled": [round(a[1], 4) for a in agree],
+        "jaccard_exact_pooled": [round(a[2], 4) for a in agree],
+    }
+
+
+def ctypes_shape(P, wl):
+    import ctypes
+    return ctypes.byref(P.Shape(wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block))
+
+
 def region_pass(P, torch, stream, sets, wl, steps):
     """The region-restricted middle-layer path on the same inputs, after the
     timed region: regions and W from a seeded evidence region, the latent
@@ -265,6 +326,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bank", action="store_true", help="skip the bit-packed mask bank pass")
     ap.add_argument("--no-region", action="store_true", help="skip the region-restricted pass")
+    ap.add_argument("--no-exact", action="store_true", help="skip the exact-mass builder pass")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before timing, copy a buffer of this size once (a reference kernel of known "
                          "traffic for hardware byte counters)")
@@ -366,6 +428,7 @@ def main():
     bank = None if args.no_bank else bank_pass(P, torch, stream, sets, flags, masks, lists, ws_mask, wl,
                                                 args.steps)
     region = None if args.no_region else region_pass(P, torch, stream, sets, wl, args.steps)
+    exact = None if args.no_exact else exact_mass_pass(P, torch, stream, sets, wl, min(args.steps, 6))
 
     # algorithmic work of one step (averaged over the rotated sets)
     fl_exec = float(np.mean([executed_flops(m.cpu().numpy(), N, bs, d) for m in masks]))
@@ -418,6 +481,8 @@ def main():
         res["mask_bank"] = bank
     if region is not None:
         res["region_restricted"] = region
+    if exact is not None:
+        res["exact_mass"] = exact
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(wl)

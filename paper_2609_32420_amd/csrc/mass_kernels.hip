@@ -8,8 +8,9 @@
 //   M[b,h,i,j] = (1 / n_i) sum_{a in block i} sum_{t in block j}
 //                softmax_t(sigma q_a . k_t)        (rows sum to 1)
 //
-// Pass 1 (mass_pass_kernel): one workgroup per query block, 32 queries per
-// wave, streams every key block of its head through LDS and computes
+// Pass 1 (mass_pass_kernel): one workgroup of 8 waves per 256 queries (two
+// blocks of 128 or four of 64), 32 queries per wave, streams every key
+// block of its head through LDS (each load serves 256 queries) and computes
 // S^T = K Q^T on bf16 MFMA 32x32x16 (fp32 accumulation), keys as MFMA rows so
 // that a query's scores sit in one lane pair.  After key block j each query
 // records (m_j, s_j): its running maximum (log2 units) and the block's
@@ -33,9 +34,28 @@ __device__ inline int mswz(int r) {
   else return (r >> 1) & 7;
 }
 
+constexpr int kMassWaves = 8;  // 256 queries per workgroup
+
+// One 32-key tile of S^T = K Q^T: K rows from LDS (row r of the tile for
+// this lane, chunks 2 t + hh), Q from registers.
+template <int D, int CPR>
+__device__ __attribute__((always_inline)) inline f32x16 qk_tile(const unsigned char *row, int r,
+                                                                int hh,
+                                                                const bf16x8 (&qreg)[D / 16]) {
+  f32x16 acc = {};
+#pragma unroll
+  for (int t = 0; t < D / 16; ++t) {
+    const int c = 2 * t + hh;
+    const bf16x8 kv = *reinterpret_cast<const bf16x8 *>(row + 16 * (c ^ mswz<CPR>(r)));
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv, qreg[t], acc, 0, 0, 0);
+  }
+  return acc;
+}
+
 template <int D, int BS>
 struct MassCfg {
-  static constexpr int NT = 2 * BS;        // BS / 32 waves of 64 lanes
+  static constexpr int QPW = kMassWaves * 32 / BS;  // query blocks per workgroup
+  static constexpr int NT = 64 * kMassWaves;
   static constexpr int CPR = D / 8;        // 16-byte chunks per K row
   static constexpr int RB = D * 2;         // bytes per K row
   static constexpr int TILE = BS * RB;     // one key block in LDS
@@ -45,18 +65,19 @@ struct MassCfg {
 };
 
 template <int D, int BS>
-__global__ void __launch_bounds__(2 * BS, 2)
+__global__ void __launch_bounds__(64 * kMassWaves)
 mass_pass_kernel(View q, View k, int H, int N, int nB, float c2, float2 *__restrict__ rec,
                  float *__restrict__ lse2) {
   using C = MassCfg<D, BS>;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
-  const int qb = (int)(blockIdx.x % nB);
-  const int bh = (int)(blockIdx.x / nB);
+  const int ng = (nB + C::QPW - 1) / C::QPW;  // query groups per head
+  const int qg = (int)(blockIdx.x % ng);
+  const int bh = (int)(blockIdx.x / ng);
   const int b = bh / H, h = bh - b * H;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int a = qb * BS + wave * 32 + l32;  // this lane's query
+  const int a = qg * (C::QPW * BS) + wave * 32 + l32;  // this lane's query
   const bool qvalid = a < N;
 
   // Q as the B operand: query l32, channels 16 t + 8 hh .. + 8
@@ -71,76 +92,95 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, float c2, float2 *__restr
   }
   const uint16_t *kbase = k.data + (int64_t)b * k.sb + (int64_t)h * k.sh;
 
-  // staged chunks of the next key block: chunk x = tid + u NT covers row
-  // x / CPR, 16-byte chunk x % CPR (rows past N read row N - 1; their scores
-  // are masked).
-  uint4 stage[C::CPT];
-#define CARNATOR_MASS_LOAD(J)                                                           \
-  _Pragma("unroll") for (int u = 0; u < C::CPT; ++u) {                                  \
-    const int x = (int)threadIdx.x + u * C::NT;                                         \
-    const int r = x / C::CPR, c = x - r * C::CPR;                                       \
-    const int tok = min((J) * BS + r, N - 1);                                           \
-    stage[u] = *reinterpret_cast<const uint4 *>(kbase + (int64_t)tok * k.sn + 8 * c);   \
+  // staged chunks of a key block: chunk x = tid + u NT covers row x / CPR,
+  // 16-byte chunk x % CPR (rows past N read row N - 1, blocks past nB - 1
+  // block nB - 1; their scores are masked or unused).
+  // Two register stages: the load of key block j + 2 is issued right after
+  // block j + 1 is stored to LDS, so it has two blocks of compute to land.
+  // The loop is unrolled by two so both stage arrays stay in registers, and
+  // runs an even number of bodies (an odd nB ends with one masked body over
+  // the LDS buffer it finds: nothing is recorded from it).
+  // (named registers, not arrays: arrays live across the loop's back edge
+  // were kept in scratch memory, each prefetch then waited for at once)
+  static_assert(C::CPT <= 4, "stage size");
+  uint4 sa0, sa1, sa2, sa3, sb0, sb1, sb2, sb3;
+#define CARNATOR_MASS_CHUNK_LOAD(V, U, J)                                                \
+  if constexpr ((U) < C::CPT) {                                                          \
+    const int x = (int)threadIdx.x + (U) * C::NT;                                        \
+    const int r = x / C::CPR, c = x - r * C::CPR;                                        \
+    const int tok = min(min(J, nB - 1) * BS + r, N - 1);                                 \
+    V = *reinterpret_cast<const uint4 *>(kbase + (int64_t)tok * k.sn + 8 * c);           \
   }
-#define CARNATOR_MASS_STORE(BUF)                                                        \
-  _Pragma("unroll") for (int u = 0; u < C::CPT; ++u) {                                  \
-    const int x = (int)threadIdx.x + u * C::NT;                                         \
-    const int r = x / C::CPR, c = x - r * C::CPR;                                       \
-    *reinterpret_cast<uint4 *>(lds + (BUF) * C::TILE + r * C::RB +                      \
-                               16 * (c ^ mswz<C::CPR>(r))) = stage[u];                  \
+#define CARNATOR_MASS_CHUNK_STORE(V, U, BUF)                                             \
+  if constexpr ((U) < C::CPT) {                                                          \
+    const int x = (int)threadIdx.x + (U) * C::NT;                                        \
+    const int r = x / C::CPR, c = x - r * C::CPR;                                        \
+    *reinterpret_cast<uint4 *>(lds + (BUF) * C::TILE + r * C::RB +                       \
+                               16 * (c ^ mswz<C::CPR>(r))) = V;                          \
   }
+#define CARNATOR_MASS_LOAD(ST, J)                                                        \
+  CARNATOR_MASS_CHUNK_LOAD(ST##0, 0, J) CARNATOR_MASS_CHUNK_LOAD(ST##1, 1, J)            \
+  CARNATOR_MASS_CHUNK_LOAD(ST##2, 2, J) CARNATOR_MASS_CHUNK_LOAD(ST##3, 3, J)
+#define CARNATOR_MASS_STORE(ST, BUF)                                                     \
+  CARNATOR_MASS_CHUNK_STORE(ST##0, 0, BUF) CARNATOR_MASS_CHUNK_STORE(ST##1, 1, BUF)      \
+  CARNATOR_MASS_CHUNK_STORE(ST##2, 2, BUF) CARNATOR_MASS_CHUNK_STORE(ST##3, 3, BUF)
 
-  CARNATOR_MASS_LOAD(0)
-  CARNATOR_MASS_STORE(0)
+  CARNATOR_MASS_LOAD(sa, 0)
+  CARNATOR_MASS_STORE(sa, 0)
+  CARNATOR_MASS_LOAD(sa, 1)
+  CARNATOR_MASS_LOAD(sb, 2)
   __syncthreads();
 
   float m_run = -INFINITY, l_run = 0.f;
-  for (int j = 0; j < nB; ++j) {
-    // unconditional (the last iteration reloads block nB - 1 into the idle
-    // buffer, which nothing reads afterwards): a load and a store under
-    // branches would keep the staging array in scratch memory
-    CARNATOR_MASS_LOAD(min(j + 1, nB - 1))
-    const unsigned char *base = lds + (j & 1) * C::TILE;
-    float x[BS / 32][16];
-#pragma unroll
-    for (int m = 0; m < BS / 32; ++m) {
-      f32x16 acc = {};
-      const int r = m * 32 + l32;
-      const unsigned char *row = base + r * C::RB;
-#pragma unroll
-      for (int t = 0; t < D / 16; ++t) {
-        const int c = 2 * t + hh;
-        const bf16x8 kv = *reinterpret_cast<const bf16x8 *>(row + 16 * (c ^ mswz<C::CPR>(r)));
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv, qreg[t], acc, 0, 0, 0);
-      }
-      // acc[v] is key 8 (v / 4) + 4 hh + (v % 4) of the tile for query l32
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = j * BS + m * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-        x[m][v] = key < N ? acc[v] * c2 : -INFINITY;
-      }
-    }
-    float mb = -INFINITY;
-#pragma unroll
-    for (int m = 0; m < BS / 32; ++m)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mb = fmaxf(mb, x[m][v]);
-    mb = fmaxf(mb, __shfl_xor(mb, 32));
-    const float m_new = fmaxf(m_run, mb);
-    float s = 0.f;
-#pragma unroll
-    for (int m = 0; m < BS / 32; ++m)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) s += exp2f(x[m][v] - m_new);
-    s += __shfl_xor(s, 32);
-    l_run = l_run * exp2f(m_run - m_new) + s;
-    m_run = m_new;
-    if (hh == 0 && qvalid) rec[((int64_t)bh * nB + j) * N + a] = make_float2(m_new, s);
-    CARNATOR_MASS_STORE((j + 1) & 1)
-    __syncthreads();
+  // one key block: LDS buffer jj & 1 holds block jj, S1 holds block jj + 1
+  // and S2 block jj + 2 (both in flight); S1 is stored for the next body and
+  // refilled with block jj + 3
+#define CARNATOR_MASS_BODY(JJ, S1)                                                       \
+  {                                                                                      \
+    const int jj = (JJ);                                                                 \
+    const bool live = jj < nB;                                                           \
+    const unsigned char *base = lds + (jj & 1) * C::TILE;                                \
+    const int lim = N - jj * BS;                                                         \
+    /* the block's maximum so far (pair-uniform) and this lane's share of the */        \
+    /* block's sum relative to it, updated tile by tile */                               \
+    float mb = m_run, sl = 0.f;                                                          \
+    _Pragma("unroll") for (int m = 0; m < BS / 32; ++m) {                                \
+      const int r = m * 32 + l32;                                                        \
+      f32x16 acc = qk_tile<D, C::CPR>(base + r * C::RB, r, hh, qreg);                    \
+      float tm = -INFINITY;                                                              \
+      _Pragma("unroll") for (int v = 0; v < 16; ++v) {                                   \
+        const int key = m * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);                        \
+        acc[v] = key < lim ? acc[v] : -INFINITY;                                         \
+        tm = fmaxf(tm, acc[v]);                                                          \
+      }                                                                                  \
+      tm = fmaxf(tm, __shfl_xor(tm, 32)) * c2;                                           \
+      const float mn = fmaxf(mb, tm);                                                    \
+      float ts = 0.f;                                                                    \
+      _Pragma("unroll") for (int v = 0; v < 16; ++v)                                     \
+        ts += __builtin_amdgcn_exp2f(fmaf(acc[v], c2, -mn));                             \
+      sl = sl * __builtin_amdgcn_exp2f(mb == -INFINITY ? -INFINITY : mb - mn) + ts;      \
+      mb = mn;                                                                           \
+    }                                                                                    \
+    const float s = sl + __shfl_xor(sl, 32);                                             \
+    if (live) {                                                                          \
+      l_run = l_run * __builtin_amdgcn_exp2f(m_run == -INFINITY ? -INFINITY : m_run - mb) + s; \
+      m_run = mb;                                                                        \
+      if (hh == 0 && qvalid) rec[((int64_t)bh * nB + jj) * N + a] = make_float2(mb, s);  \
+    }                                                                                    \
+    CARNATOR_MASS_STORE(S1, (jj + 1) & 1)                                                \
+    __syncthreads();                                                                     \
+    CARNATOR_MASS_LOAD(S1, jj + 3)                                                       \
   }
+
+  for (int j = 0; j < nB; j += 2) {
+    CARNATOR_MASS_BODY(j, sa)
+    CARNATOR_MASS_BODY(j + 1, sb)
+  }
+#undef CARNATOR_MASS_BODY
 #undef CARNATOR_MASS_LOAD
 #undef CARNATOR_MASS_STORE
+#undef CARNATOR_MASS_CHUNK_LOAD
+#undef CARNATOR_MASS_CHUNK_STORE
   if (hh == 0 && qvalid) lse2[(int64_t)bh * N + a] = m_run + log2f(l_run);
 }
 
@@ -181,7 +221,8 @@ hipError_t launch_mass(View q, View k, int B, int H, int N, int d, int bs, float
   float *lse2 = reinterpret_cast<float *>(static_cast<char *>(scratch) +
                                           align_up((size_t)BH * nB * N * sizeof(float2)));
   const float c2 = scale * 1.4426950408889634f;
-  const dim3 grid((unsigned)(BH * nB));
+  const int qpw = kMassWaves * 32 / bs;
+  const dim3 grid((unsigned)(BH * ((nB + qpw - 1) / qpw)));
   hipError_t e = hipSuccess;
 #define CARNATOR_MASS(DD, BB)                                                                   \
   do {                                                                                          \
