@@ -28,6 +28,10 @@ region, the latent blend (HBM-bound; its GB/s against the 8 TB/s peak),
 block flags, compaction restricted to active rows and context keys, and
 the attention of the active rows only -- each timed alone.
 
+After the timed steps the attention is also timed with its compaction, as
+one mask-in call (``attn_with_compaction_ms_per_call``); the timed steps'
+attention launches give ``attn_ms_p10_p50_p90``.
+
 ``exact_mass`` (after the timed region, skipped with --no-exact): the
 builder on the token-level attention mass -- the dense mass pass against
 the bf16 MFMA peak and the selection on its masses -- with the exact masks
@@ -425,6 +429,23 @@ def main():
     def avg_ms(name):
         return float(np.mean([a.elapsed_time(b) for a, b in ev[name]]))
 
+    # the attention timed with its compaction: one mask-in call
+    # (carnator_block_sparse_attn: compaction + attention), events around it
+    ws_attn = P.block_sparse_attn_workspace(sets[0][0]["q"], bs)
+    with_cmp = []
+    for i in range(args.steps + 1):
+        si = i % len(sets)
+        x = sets[si][0]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        P.block_sparse_attn(x["q"], x["k"], x["v"], masks[si], bs, out=outs[si], workspace=ws_attn)
+        e1.record(stream)
+        if i > 0:
+            with_cmp.append((e0, e1))
+    torch.cuda.synchronize()
+    attn_times = np.array([a.elapsed_time(b) for a, b in ev["attn"]])
+    with_cmp_ms = float(np.mean([a.elapsed_time(b) for a, b in with_cmp]))
+
     bank = None if args.no_bank else bank_pass(P, torch, stream, sets, flags, masks, lists, ws_mask, wl,
                                                 args.steps)
     region = None if args.no_region else region_pass(P, torch, stream, sets, wl, args.steps)
@@ -458,6 +479,8 @@ def main():
                    "signature_bank": [synth.SIG_M, synth.SIG_D], "topk": synth.SIG_TOPK,
                    "input_sets": len(sets), "parallelism": "none (1 GPU)"},
         "attn_ms_per_call": round(attn_ms, 4),
+        "attn_ms_p10_p50_p90": [round(float(np.percentile(attn_times, p_)), 4) for p_ in (10, 50, 90)],
+        "attn_with_compaction_ms_per_call": round(with_cmp_ms, 4),
         "attn_executed_tflop": round(fl_exec / 1e12, 4),
         "attn_dense_equiv_tflop": round(fl_dense / 1e12, 4),
         "attn_executed_tflops": round(attn_tflops, 2),
