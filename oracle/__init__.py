@@ -28,6 +28,9 @@ Every function is plain fp64 NumPy, written from the paper's definitions:
 * ``exact_block_mass`` / ``select_row_mass`` / ``mask_from_mass``: the
   token-level attention mass of each block pair and the selection on it
   (Appendix C.3, "source attention mass" read literally).
+* ``ciede2000`` / ``support_area`` / ``normalized_shape`` / ``d_size`` /
+  ``d_shape`` / ``gate`` / ``first_compatible`` / ``clopper_pearson_upper``:
+  the compatibility gate of a recalled cache (Sec. 3.2; Appendix F).
 * ``block_sparse_attention``: softmax attention of the recomputed target
   Q, K, V restricted to the reused block structure (Sec. 3.3, "Historical
   Sparse-Connectivity Reuse"; Appendix C.3).
@@ -42,6 +45,8 @@ from .mask import (pool_blocks, block_scores, select_row, build_block_mask,
                    merge_target_rows, compact_mask, row_admissible_masks, TIE_EPS,
                    FRAGILE_EPS, pack_mask, unpack_mask)
 from .attention import block_sparse_attention, token_mask_from_blocks
+from .gate import (ciede2000, support_area, normalized_shape, d_size, d_shape, gate, first_compatible,
+                   clopper_pearson_upper, SHAPE_RES)
 from .exact_mass import exact_block_mass, select_row_mass, mask_from_mass
 from .region import (dilate_frames, chebyshev_distance, smoothstep, regions, latent_fusion,
                      region_block_flags, restrict_mask, compact_restricted)
@@ -56,4 +61,6 @@ __all__ = [
     "dilate_frames", "chebyshev_distance", "smoothstep", "regions", "latent_fusion",
     "region_block_flags", "restrict_mask", "compact_restricted",
     "exact_block_mass", "select_row_mass", "mask_from_mass",
+    "ciede2000", "support_area", "normalized_shape", "d_size", "d_shape", "gate", "first_compatible",
+    "clopper_pearson_upper", "SHAPE_RES",
 ]
