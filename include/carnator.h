@@ -28,6 +28,12 @@
  *                               (Sec. 3.3, region-guided latent reuse and
  *                               joint reuse in intermediate layers; Appendix
  *                               C.3)
+ *   carnator_ciede2000, carnator_shape_descriptor,
+ *   carnator_object_discrepancy, carnator_compat_gate,
+ *   carnator_clopper_pearson_upper
+ *                               the compatibility gate of a recalled cache
+ *                               and its certification (Sec. 3.2, Appendix
+ *                               F); host code
  *   carnator_signature_sim      cosine scoring of an early-step signature
  *                               against a bank of cached signatures (Sec. 3.1,
  *                               Sec. 4.1 candidate recall)
@@ -78,7 +84,7 @@
 extern "C" {
 #endif
 
-#define CARNATOR_ABI_VERSION 4
+#define CARNATOR_ABI_VERSION 5
 
 typedef enum {
   CARNATOR_OK = 0,
@@ -218,6 +224,51 @@ int carnator_block_mass_exact(const carnator_view *q_hist, const carnator_view *
 int carnator_select_block_mask(const double *mass, const carnator_shape *shape,
                                double mass_threshold, uint8_t *mask_out, uint64_t *bits_out,
                                hipStream_t stream);
+
+/*
+ * Compatibility gate -- Sec. 3.2 ("Reuse Validity with Generation-Native
+ * Evidence": compatibility filtering and risk-aware compatibility decisions)
+ * and Appendix F.  Per object the Early Signature holds the normalised
+ * support size A of its binary tail-frame mask (the mean over the H x W
+ * grid), the mask and a CIELAB colour.  Against a candidate:
+ *   d_size  = |ln(A_q / A_j)|  (0 if both areas are 0, +inf if one is),
+ *   d_shape = 1 - 2 |S_q and S_j| / (|S_q| + |S_j|) over the masks cropped
+ *             to their bounding boxes and resampled to res x res (0 if both
+ *             are empty),
+ *   d_color = CIEDE2000 (kL = kC = kH = 1); d_context is the largest
+ *             CIEDE2000 over the objects both requests share.
+ * A candidate passes when every discrepancy is within its threshold; the
+ * first passing candidate in recall order is reused, else the request runs
+ * dense.  A threshold setting is certified by the one-sided Clopper-Pearson
+ * upper bound U_alpha(u, n) on the unsafe-reuse rate.
+ *
+ * All of these run on the host, on HOST pointers, and enqueue nothing.
+ *
+ * carnator_ciede2000: out[i] = CIEDE2000(lab1[i], lab2[i]); lab1, lab2
+ *   double [n][3] (L, a, b); out double [n].
+ * carnator_shape_descriptor: area = mean of mask != 0; shape uint8
+ *   [res][res] = the bounding-box crop (h x w) sampled at source row
+ *   floor((y + 0.5) h / res), column floor((x + 0.5) w / res); all 0 for an
+ *   empty mask.  mask uint8 [height][width].
+ * carnator_object_discrepancy: d double [3] = (d_size, d_shape, d_color) of
+ *   one object; shapes uint8 [res][res], colours double [3].
+ * carnator_compat_gate: d double [n_candidates][n_terms] in recall order,
+ *   tau double [n_terms]; *chosen = the first candidate with d <= tau in
+ *   every term, or -1.
+ * carnator_clopper_pearson_upper: *upper = the p at which the probability of
+ *   at most u failures in n Bernoulli(p) trials equals alpha (1 when u = n);
+ *   0 <= u <= n, n >= 1, 0 < alpha < 1.
+ * Errors: E_NULL, E_SHAPE.
+ */
+int carnator_ciede2000(const double *lab1, const double *lab2, int64_t n, double *out);
+int carnator_shape_descriptor(const uint8_t *mask, int32_t height, int32_t width, int32_t res,
+                              double *area, uint8_t *shape);
+int carnator_object_discrepancy(double area_q, double area_j, const uint8_t *shape_q,
+                                const uint8_t *shape_j, int32_t res, const double *lab_q,
+                                const double *lab_j, double *d);
+int carnator_compat_gate(const double *d, int64_t n_candidates, int32_t n_terms, const double *tau,
+                         int32_t *chosen);
+int carnator_clopper_pearson_upper(int64_t u, int64_t n, double alpha, double *upper);
 
 /*
  * Bit-packed masks: the historical block connectivity in its stored form.

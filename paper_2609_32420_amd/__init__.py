@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libcarnator.so")
 
 CARNATOR_OK = 0
 # CARNATOR_ABI_VERSION of include/carnator.h this binding marshals for
-ABI_VERSION = 4
+ABI_VERSION = 5
 STATUS = {0: "OK", -1: "E_NULL", -2: "E_SHAPE", -3: "E_UNSUPPORTED", -4: "E_ALIGN",
           -5: "E_WORKSPACE", -6: "E_HIP"}
 
@@ -38,6 +38,8 @@ EXPORTS = (
     "carnator_block_sparse_attn_workspace_size", "carnator_block_sparse_attn",
     "carnator_block_sparse_attn_lists",
     "carnator_signature_sim_workspace_size", "carnator_signature_sim",
+    "carnator_ciede2000", "carnator_shape_descriptor", "carnator_object_discrepancy", "carnator_compat_gate",
+    "carnator_clopper_pearson_upper",
 )
 
 
@@ -101,6 +103,11 @@ def lib() -> ctypes.CDLL:
                                                                 P, P]),
             "carnator_signature_sim_workspace_size": (SZ, [I64, I64, I32]),
             "carnator_signature_sim": (ctypes.c_int, [P, I64, P, I64, I64, I64, I32, P, P, P, P, SZ, P]),
+            "carnator_ciede2000": (ctypes.c_int, [P, P, I64, P]),
+            "carnator_shape_descriptor": (ctypes.c_int, [P, I32, I32, I32, P, P]),
+            "carnator_object_discrepancy": (ctypes.c_int, [F64, F64, P, P, I32, P, P, P]),
+            "carnator_compat_gate": (ctypes.c_int, [P, I64, I32, P, P]),
+            "carnator_clopper_pearson_upper": (ctypes.c_int, [I64, I64, F64, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(L, name)
@@ -609,3 +616,78 @@ def signature_sim(query: torch.Tensor, bank: torch.Tensor, topk: int, return_all
     _check(L.carnator_signature_sim(_ptr(query), nq, _ptr(bank), m, dim, bank.stride(0), int(topk), _ptr(idx),
                                     _ptr(sim), _ptr(allsim), _ptr(workspace), workspace.numel(), _stream(query)))
     return (idx, sim, allsim) if return_all else (idx, sim)
+
+
+# ---------------------------------------------------------------- compatibility gate (host)
+#
+# Host code on NumPy arrays: a handful of objects and candidates per request.
+
+def _host(a, dtype, shape=None):
+    import numpy as np
+    a = np.ascontiguousarray(a, dtype=dtype)
+    if shape is not None and a.shape != tuple(shape):
+        raise ValueError("expected shape %s, got %s" % (tuple(shape), a.shape))
+    return a
+
+
+def _hp(a):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def ciede2000(lab1, lab2):
+    """CIEDE2000 of [..., 3] CIELAB arrays (carnator_ciede2000)."""
+    import numpy as np
+    a = _host(lab1, np.float64)
+    b = _host(lab2, np.float64)
+    if a.shape != b.shape or a.shape[-1] != 3:
+        raise ValueError("lab1 and lab2 must have the same [..., 3] shape")
+    out = np.empty(a.shape[:-1], dtype=np.float64)
+    _check(lib().carnator_ciede2000(_hp(a), _hp(b), out.size, _hp(out)))
+    return out
+
+
+def shape_descriptor(mask, res: int = 32):
+    """(area, normalised shape uint8 [res, res]) of a binary tail-frame mask
+    (carnator_shape_descriptor)."""
+    import numpy as np
+    m = _host(np.asarray(mask) != 0, np.uint8)
+    if m.ndim != 2:
+        raise ValueError("mask must be [H, W]")
+    area = np.zeros(1, dtype=np.float64)
+    shape = np.zeros((res, res), dtype=np.uint8)
+    _check(lib().carnator_shape_descriptor(_hp(m), m.shape[0], m.shape[1], res, _hp(area), _hp(shape)))
+    return float(area[0]), shape
+
+
+def object_discrepancy(area_q, area_j, shape_q, shape_j, lab_q, lab_j):
+    """(d_size, d_shape, d_color) of one object (carnator_object_discrepancy)."""
+    import numpy as np
+    sq = _host(shape_q, np.uint8)
+    sj = _host(shape_j, np.uint8, sq.shape)
+    lq = _host(lab_q, np.float64, (3,))
+    lj = _host(lab_j, np.float64, (3,))
+    d = np.zeros(3, dtype=np.float64)
+    _check(lib().carnator_object_discrepancy(float(area_q), float(area_j), _hp(sq), _hp(sj), sq.shape[0], _hp(lq),
+                                             _hp(lj), _hp(d)))
+    return d
+
+
+def compat_gate(d_candidates, tau) -> int:
+    """First candidate (recall order) with every discrepancy within its
+    threshold, or -1 (carnator_compat_gate)."""
+    import numpy as np
+    d = _host(d_candidates, np.float64)
+    t = _host(tau, np.float64)
+    if d.ndim != 2 or d.shape[1] != t.size:
+        raise ValueError("d must be [n_candidates, len(tau)]")
+    chosen = np.zeros(1, dtype=np.int32)
+    _check(lib().carnator_compat_gate(_hp(d), d.shape[0], t.size, _hp(t), _hp(chosen)))
+    return int(chosen[0])
+
+
+def clopper_pearson_upper(u: int, n: int, alpha: float) -> float:
+    """One-sided Clopper-Pearson upper bound (carnator_clopper_pearson_upper)."""
+    import numpy as np
+    out = np.zeros(1, dtype=np.float64)
+    _check(lib().carnator_clopper_pearson_upper(int(u), int(n), float(alpha), _hp(out)))
+    return float(out[0])

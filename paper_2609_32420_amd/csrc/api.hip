@@ -535,3 +535,97 @@ int carnator_signature_sim(const float *query, int64_t nq, const float *bank, in
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------- compatibility gate (host)
+
+int carnator_ciede2000(const double *lab1, const double *lab2, int64_t n, double *out) {
+  if (!lab1 || !lab2 || !out) return fail(CARNATOR_E_NULL, "lab1, lab2 and out must be non-NULL");
+  if (n < 0) return fail(CARNATOR_E_SHAPE, "n must be >= 0");
+  for (int64_t i = 0; i < n; ++i) out[i] = ciede2000_pair(lab1 + 3 * i, lab2 + 3 * i);
+  return ok();
+}
+
+int carnator_shape_descriptor(const uint8_t *mask, int32_t height, int32_t width, int32_t res,
+                              double *area, uint8_t *shape) {
+  if (!mask || !area || !shape) return fail(CARNATOR_E_NULL, "mask, area and shape must be non-NULL");
+  if (height < 1 || width < 1 || res < 1) return fail(CARNATOR_E_SHAPE, "height, width and res must be >= 1");
+  int y0 = height, y1 = -1, x0 = width, x1 = -1;
+  int64_t cnt = 0;
+  for (int y = 0; y < height; ++y)
+    for (int x = 0; x < width; ++x)
+      if (mask[(int64_t)y * width + x]) {
+        ++cnt;
+        y0 = y < y0 ? y : y0, y1 = y > y1 ? y : y1;
+        x0 = x < x0 ? x : x0, x1 = x > x1 ? x : x1;
+      }
+  *area = (double)cnt / ((double)height * width);
+  for (int64_t i = 0; i < (int64_t)res * res; ++i) shape[i] = 0;
+  if (cnt == 0) return ok();
+  const int h = y1 - y0 + 1, w = x1 - x0 + 1;
+  for (int y = 0; y < res; ++y) {
+    // floor((y + 0.5) h / res) = (2 y + 1) h / (2 res) in integers
+    const int sy = (int)(((int64_t)(2 * y + 1) * h) / (2 * (int64_t)res));
+    for (int x = 0; x < res; ++x) {
+      const int sx = (int)(((int64_t)(2 * x + 1) * w) / (2 * (int64_t)res));
+      shape[(int64_t)y * res + x] = mask[(int64_t)(y0 + sy) * width + (x0 + sx)] ? 1 : 0;
+    }
+  }
+  return ok();
+}
+
+int carnator_object_discrepancy(double area_q, double area_j, const uint8_t *shape_q,
+                                const uint8_t *shape_j, int32_t res, const double *lab_q,
+                                const double *lab_j, double *d) {
+  if (!shape_q || !shape_j || !lab_q || !lab_j || !d)
+    return fail(CARNATOR_E_NULL, "shapes, colours and d must be non-NULL");
+  if (res < 1 || !(area_q >= 0.0) || !(area_j >= 0.0))
+    return fail(CARNATOR_E_SHAPE, "res must be >= 1 and the areas >= 0");
+  if (area_q == 0.0 && area_j == 0.0) d[0] = 0.0;
+  else if (area_q == 0.0 || area_j == 0.0) d[0] = INFINITY;
+  else d[0] = fabs(log(area_q / area_j));
+  int64_t inter = 0, tot = 0;
+  for (int64_t i = 0; i < (int64_t)res * res; ++i) {
+    const bool a = shape_q[i] != 0, b = shape_j[i] != 0;
+    inter += a && b;
+    tot += (int)a + (int)b;
+  }
+  d[1] = tot == 0 ? 0.0 : 1.0 - 2.0 * (double)inter / (double)tot;
+  d[2] = ciede2000_pair(lab_q, lab_j);
+  return ok();
+}
+
+int carnator_compat_gate(const double *d, int64_t n_candidates, int32_t n_terms, const double *tau,
+                         int32_t *chosen) {
+  if (!d || !tau || !chosen) return fail(CARNATOR_E_NULL, "d, tau and chosen must be non-NULL");
+  if (n_candidates < 0 || n_terms < 1) return fail(CARNATOR_E_SHAPE, "bad candidate or term count");
+  *chosen = -1;
+  for (int64_t c = 0; c < n_candidates; ++c) {
+    bool pass = true;
+    for (int k = 0; k < n_terms; ++k) pass = pass && d[c * n_terms + k] <= tau[k];
+    if (pass) {
+      *chosen = (int32_t)c;
+      break;
+    }
+  }
+  return ok();
+}
+
+int carnator_clopper_pearson_upper(int64_t u, int64_t n, double alpha, double *upper) {
+  if (!upper) return fail(CARNATOR_E_NULL, "upper is NULL");
+  if (n < 1 || u < 0 || u > n) return fail(CARNATOR_E_SHAPE, "need 0 <= u <= n and n >= 1");
+  if (!(alpha > 0.0 && alpha < 1.0)) return fail(CARNATOR_E_SHAPE, "alpha must lie in (0, 1)");
+  if (u == n) {
+    *upper = 1.0;
+    return ok();
+  }
+  const double la = log(alpha);
+  double lo = 0.0, hi = 1.0;
+  for (int it = 0; it < 200 && hi - lo > 0.0; ++it) {
+    const double mid = 0.5 * (lo + hi);
+    if (mid <= lo || mid >= hi) break;
+    if (log_binom_tail(u, n, mid) > la) lo = mid;  // tail still above alpha: p larger
+    else hi = mid;
+  }
+  *upper = 0.5 * (lo + hi);
+  return ok();
+}

@@ -149,6 +149,12 @@ hipError_t launch_fusion(const float *zt, const float *zh, const float *weight, 
 hipError_t launch_block_flags(const uint8_t *region, int B, int n_text, int N, int bs, uint8_t *act,
                               uint8_t *ctx, hipStream_t s);
 
+// ---- compatibility gate (host code) -------------------------------------------
+// CIEDE2000 of two CIELAB colours (3 doubles each), kL = kC = kH = 1.
+double ciede2000_pair(const double *lab1, const double *lab2);
+// log P(X <= u) for X ~ Binomial(n, p), 0 < p < 1.
+double log_binom_tail(int64_t u, int64_t n, double p);
+
 // ---- attention -------------------------------------------------------------
 // Rows order[0 .. *n_rows) when n_rows is not NULL, else all B H nB rows.
 hipError_t launch_bsattn(View q, View k, View v, uint16_t *out, int64_t osb, int64_t osh,
