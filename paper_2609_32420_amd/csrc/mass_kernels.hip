@@ -8,9 +8,10 @@
 //   M[b,h,i,j] = (1 / n_i) sum_{a in block i} sum_{t in block j}
 //                softmax_t(sigma q_a . k_t)        (rows sum to 1)
 //
-// Pass 1 (mass_pass_kernel): one workgroup of 8 waves per 256 queries (two
-// blocks of 128 or four of 64), 32 queries per wave, streams every key
-// block of its head through LDS (each load serves 256 queries) and computes
+// Pass 1 (mass_pass_kernel): one workgroup of 8 waves per 512 queries (four
+// blocks of 128 or eight of 64), 64 queries per wave in two sets of 32 (each
+// K operand read from LDS feeds two MFMAs), streams every key block of its
+// head through LDS (each load serves 512 queries) and computes
 // S^T = K Q^T on bf16 MFMA 32x32x16 (fp32 accumulation), keys as MFMA rows so
 // that a query's scores sit in one lane pair.  After key block j each query
 // records (m_j, s_j): its running maximum (log2 units) and the block's
@@ -34,27 +35,56 @@ __device__ inline int mswz(int r) {
   else return (r >> 1) & 7;
 }
 
-constexpr int kMassWaves = 8;  // 256 queries per workgroup
+constexpr int kMassWaves = 8;  // 64 queries per wave, 512 per workgroup
+constexpr int kMassQueries = 64 * kMassWaves;
 
-// One 32-key tile of S^T = K Q^T: K rows from LDS (row r of the tile for
-// this lane, chunks 2 t + hh), Q from registers.
+// Softmax statistics of one query (pair-uniform): the running maximum and
+// sum over the key blocks done, and the current block's maximum and this
+// lane's share of its sum.
+struct MassState {
+  float m_run, l_run, mb, sl;
+};
+
+// Fold one 32-key tile of scores (raw, keys at or past lim masked) into st.
+__device__ __attribute__((always_inline)) inline void mass_tile(MassState &st, f32x16 acc, int m,
+                                                                int hh, int lim, float c2) {
+  float tm = -INFINITY;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int key = m * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
+    acc[v] = key < lim ? acc[v] : -INFINITY;
+    tm = fmaxf(tm, acc[v]);
+  }
+  tm = fmaxf(tm, __shfl_xor(tm, 32)) * c2;
+  const float mn = fmaxf(st.mb, tm);
+  float ts = 0.f;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) ts += __builtin_amdgcn_exp2f(fmaf(acc[v], c2, -mn));
+  st.sl = st.sl * __builtin_amdgcn_exp2f(st.mb == -INFINITY ? -INFINITY : st.mb - mn) + ts;
+  st.mb = mn;
+}
+
+// One 32-key tile of S^T = K Q^T for both query sets: each K operand (row r
+// of the tile for this lane, chunks 2 t + hh, from LDS) feeds two MFMAs.
 template <int D, int CPR>
-__device__ __attribute__((always_inline)) inline f32x16 qk_tile(const unsigned char *row, int r,
-                                                                int hh,
-                                                                const bf16x8 (&qreg)[D / 16]) {
-  f32x16 acc = {};
+__device__ __attribute__((always_inline)) inline void qk_tile2(const unsigned char *row, int r,
+                                                                int hh, const bf16x8 (&q0)[D / 16],
+                                                                const bf16x8 (&q1)[D / 16],
+                                                                f32x16 &acc0, f32x16 &acc1) {
+  acc0 = f32x16{};
+  acc1 = f32x16{};
 #pragma unroll
   for (int t = 0; t < D / 16; ++t) {
     const int c = 2 * t + hh;
     const bf16x8 kv = *reinterpret_cast<const bf16x8 *>(row + 16 * (c ^ mswz<CPR>(r)));
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv, qreg[t], acc, 0, 0, 0);
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv, q0[t], acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kv, q1[t], acc1, 0, 0, 0);
   }
-  return acc;
 }
 
 template <int D, int BS>
 struct MassCfg {
-  static constexpr int QPW = kMassWaves * 32 / BS;  // query blocks per workgroup
+  static constexpr int QPW = kMassQueries / BS;  // query blocks per workgroup
   static constexpr int NT = 64 * kMassWaves;
   static constexpr int CPR = D / 8;        // 16-byte chunks per K row
   static constexpr int RB = D * 2;         // bytes per K row
@@ -77,17 +107,22 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, float c2, float2 *__restr
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const int a = qg * (C::QPW * BS) + wave * 32 + l32;  // this lane's query
-  const bool qvalid = a < N;
+  // this lane's two queries: l32 of each of the wave's two sets of 32
+  const int a0 = qg * kMassQueries + wave * 64 + l32, a1 = a0 + 32;
+  const bool qv0 = a0 < N, qv1 = a1 < N;
 
-  // Q as the B operand: query l32, channels 16 t + 8 hh .. + 8
-  bf16x8 qreg[D / 16];
+  // Q as the B operand: query l32 of a set, channels 16 t + 8 hh .. + 8
+  bf16x8 q0[D / 16], q1[D / 16];
   {
-    const uint16_t *qp = q.data + (int64_t)b * q.sb + (int64_t)h * q.sh + (int64_t)min(a, N - 1) * q.sn;
+    const uint16_t *qh = q.data + (int64_t)b * q.sb + (int64_t)h * q.sh;
+    const uint16_t *p0 = qh + (int64_t)min(a0, N - 1) * q.sn;
+    const uint16_t *p1 = qh + (int64_t)min(a1, N - 1) * q.sn;
 #pragma unroll
     for (int t = 0; t < D / 16; ++t) {
-      const uint4 v = *reinterpret_cast<const uint4 *>(qp + 16 * t + 8 * hh);
-      qreg[t] = qvalid ? __builtin_bit_cast(bf16x8, v) : bf16x8{};
+      const uint4 v0 = *reinterpret_cast<const uint4 *>(p0 + 16 * t + 8 * hh);
+      const uint4 v1 = *reinterpret_cast<const uint4 *>(p1 + 16 * t + 8 * hh);
+      q0[t] = qv0 ? __builtin_bit_cast(bf16x8, v0) : bf16x8{};
+      q1[t] = qv1 ? __builtin_bit_cast(bf16x8, v1) : bf16x8{};
     }
   }
   const uint16_t *kbase = k.data + (int64_t)b * k.sb + (int64_t)h * k.sh;
@@ -131,7 +166,7 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, float c2, float2 *__restr
   CARNATOR_MASS_LOAD(sb, 2)
   __syncthreads();
 
-  float m_run = -INFINITY, l_run = 0.f;
+  MassState s0 = {-INFINITY, 0.f, -INFINITY, 0.f}, s1 = s0;
   // one key block: LDS buffer jj & 1 holds block jj, S1 holds block jj + 1
   // and S2 block jj + 2 (both in flight); S1 is stored for the next body and
   // refilled with block jj + 3
@@ -141,31 +176,23 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, float c2, float2 *__restr
     const bool live = jj < nB;                                                           \
     const unsigned char *base = lds + (jj & 1) * C::TILE;                                \
     const int lim = N - jj * BS;                                                         \
-    /* the block's maximum so far (pair-uniform) and this lane's share of the */        \
-    /* block's sum relative to it, updated tile by tile */                               \
-    float mb = m_run, sl = 0.f;                                                          \
+    s0.mb = s0.m_run, s0.sl = 0.f, s1.mb = s1.m_run, s1.sl = 0.f;                        \
     _Pragma("unroll") for (int m = 0; m < BS / 32; ++m) {                                \
       const int r = m * 32 + l32;                                                        \
-      f32x16 acc = qk_tile<D, C::CPR>(base + r * C::RB, r, hh, qreg);                    \
-      float tm = -INFINITY;                                                              \
-      _Pragma("unroll") for (int v = 0; v < 16; ++v) {                                   \
-        const int key = m * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);                        \
-        acc[v] = key < lim ? acc[v] : -INFINITY;                                         \
-        tm = fmaxf(tm, acc[v]);                                                          \
-      }                                                                                  \
-      tm = fmaxf(tm, __shfl_xor(tm, 32)) * c2;                                           \
-      const float mn = fmaxf(mb, tm);                                                    \
-      float ts = 0.f;                                                                    \
-      _Pragma("unroll") for (int v = 0; v < 16; ++v)                                     \
-        ts += __builtin_amdgcn_exp2f(fmaf(acc[v], c2, -mn));                             \
-      sl = sl * __builtin_amdgcn_exp2f(mb == -INFINITY ? -INFINITY : mb - mn) + ts;      \
-      mb = mn;                                                                           \
+      f32x16 acc0, acc1;                                                                 \
+      qk_tile2<D, C::CPR>(base + r * C::RB, r, hh, q0, q1, acc0, acc1);                  \
+      mass_tile(s0, acc0, m, hh, lim, c2);                                               \
+      mass_tile(s1, acc1, m, hh, lim, c2);                                               \
     }                                                                                    \
-    const float s = sl + __shfl_xor(sl, 32);                                             \
+    const float t0 = s0.sl + __shfl_xor(s0.sl, 32), t1 = s1.sl + __shfl_xor(s1.sl, 32);  \
     if (live) {                                                                          \
-      l_run = l_run * __builtin_amdgcn_exp2f(m_run == -INFINITY ? -INFINITY : m_run - mb) + s; \
-      m_run = mb;                                                                        \
-      if (hh == 0 && qvalid) rec[((int64_t)bh * nB + jj) * N + a] = make_float2(mb, s);  \
+      s0.l_run = s0.l_run * __builtin_amdgcn_exp2f(s0.m_run == -INFINITY ? -INFINITY : s0.m_run - s0.mb) + t0; \
+      s0.m_run = s0.mb;                                                                  \
+      s1.l_run = s1.l_run * __builtin_amdgcn_exp2f(s1.m_run == -INFINITY ? -INFINITY : s1.m_run - s1.mb) + t1; \
+      s1.m_run = s1.mb;                                                                  \
+      float2 *rj = rec + ((int64_t)bh * nB + jj) * N;                                    \
+      if (hh == 0 && qv0) rj[a0] = make_float2(s0.mb, t0);                               \
+      if (hh == 0 && qv1) rj[a1] = make_float2(s1.mb, t1);                               \
     }                                                                                    \
     CARNATOR_MASS_STORE(S1, (jj + 1) & 1)                                                \
     __syncthreads();                                                                     \
@@ -181,7 +208,8 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, float c2, float2 *__restr
 #undef CARNATOR_MASS_STORE
 #undef CARNATOR_MASS_CHUNK_LOAD
 #undef CARNATOR_MASS_CHUNK_STORE
-  if (hh == 0 && qvalid) lse2[(int64_t)bh * N + a] = m_run + log2f(l_run);
+  if (hh == 0 && qv0) lse2[(int64_t)bh * N + a0] = s0.m_run + log2f(s0.l_run);
+  if (hh == 0 && qv1) lse2[(int64_t)bh * N + a1] = s1.m_run + log2f(s1.l_run);
 }
 
 // One wave per (bh, i, j): M_ij = sum over the valid queries a of block i of
@@ -221,7 +249,7 @@ hipError_t launch_mass(View q, View k, int B, int H, int N, int d, int bs, float
   float *lse2 = reinterpret_cast<float *>(static_cast<char *>(scratch) +
                                           align_up((size_t)BH * nB * N * sizeof(float2)));
   const float c2 = scale * 1.4426950408889634f;
-  const int qpw = kMassWaves * 32 / bs;
+  const int qpw = kMassQueries / bs;
   const dim3 grid((unsigned)(BH * ((nB + qpw - 1) / qpw)));
   hipError_t e = hipSuccess;
 #define CARNATOR_MASS(DD, BB)                                                                   \
