@@ -106,3 +106,20 @@ def test_selection_on_equal_masses(nb, tau):
     want = np.zeros(nb, np.uint8)
     want[:k] = 1
     assert (got == want).all()
+
+
+# every launch shape of the selection's mass mode: nB <= 512 (16 rows, 16
+# waves), <= 1024 (16 rows, 8 waves), up to 2048 (8 rows, 8 waves), with
+# masses that repeat exactly (ties at the cut)
+@pytest.mark.parametrize("nb,tau", [(1, 0.9), (63, 0.5), (700, 0.9), (1025, 0.8), (2048, 0.95)])
+def test_selection_on_synthetic_masses_all_launch_shapes(nb, tau):
+    rng = np.random.default_rng(nb)
+    m = rng.random((1, 2, nb, nb)) ** 6
+    m[..., ::7] = m[..., :1]  # exact repeats of the first mass in every row
+    m /= m.sum(axis=-1, keepdims=True)
+    want, rep = oracle.mask_from_mass(m, tau)
+    got = P.select_block_mask(torch.as_tensor(m, device=DEV), tau).cpu().numpy()
+    bad = [tuple(r) for r in np.argwhere((got != want).any(axis=-1))]
+    assert set(bad) <= set(rep["fragile"]), bad[:5]
+    bits = P.select_block_mask(torch.as_tensor(m, device=DEV), tau, bits=True).cpu().numpy().view(np.uint64)
+    np.testing.assert_array_equal(bits, oracle.pack_mask(got))
