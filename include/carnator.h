@@ -202,8 +202,15 @@ int carnator_compact_block_mask(const uint8_t *mask, const carnator_shape *shape
  *   q_hist, k_hist  bf16 views [B, H, N, d]
  *   mass            fp64 [B, H, nB, nB] out
  *   workspace       carnator_block_mass_exact_workspace_size(shape) bytes,
- *                   256-byte aligned (8 B per (query, key block) plus 4 B
- *                   per query: 0.8 GB at B=1, H=12, N=32,760, block 128)
+ *                   256-byte aligned: 8 B per (query, key block) plus 4 B
+ *                   per query for each head of a chunk.  Heads are processed
+ *                   in chunks whose records fit in 4 GiB (at least one head
+ *                   per chunk), so the workspace is at most
+ *                   max(4 GiB, one head's records): 0.81 GB at B=1, H=12,
+ *                   N=32,760, block 128 (all heads in one chunk), 3.55 GB
+ *                   at H=24, N=119,056 (4 heads per chunk, 6 chunks),
+ *                   4.3 GB for one head at the largest N (2048 blocks of
+ *                   128).  A smaller workspace gives E_WORKSPACE.
  * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_WORKSPACE, E_HIP.
  *
  * carnator_select_block_mask: the selection of carnator_build_block_mask

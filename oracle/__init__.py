@@ -47,7 +47,7 @@ from .mask import (pool_blocks, block_scores, select_row, build_block_mask,
 from .attention import block_sparse_attention, token_mask_from_blocks
 from .gate import (ciede2000, support_area, normalized_shape, d_size, d_shape, gate, first_compatible,
                    clopper_pearson_upper, SHAPE_RES)
-from .exact_mass import exact_block_mass, select_row_mass, mask_from_mass
+from .exact_mass import exact_block_mass, select_row_mass, mask_from_mass, row_admissible_masks_mass
 from .region import (dilate_frames, chebyshev_distance, smoothstep, regions, latent_fusion,
                      region_block_flags, restrict_mask, compact_restricted)
 from .cosine import cosine_similarity, topk_cosine
@@ -60,7 +60,7 @@ __all__ = [
     "cosine_similarity", "topk_cosine", "to_f64",
     "dilate_frames", "chebyshev_distance", "smoothstep", "regions", "latent_fusion",
     "region_block_flags", "restrict_mask", "compact_restricted",
-    "exact_block_mass", "select_row_mass", "mask_from_mass",
+    "exact_block_mass", "select_row_mass", "mask_from_mass", "row_admissible_masks_mass",
     "ciede2000", "support_area", "normalized_shape", "d_size", "d_shape", "gate", "first_compatible",
     "clopper_pearson_upper", "SHAPE_RES",
 ]

@@ -65,6 +65,29 @@ def select_row_mass(m: np.ndarray, tau: float, tie_eps: float = TIE_EPS) -> dict
     return {"keep": keep, "k": k, "fragile": fragile}
 
 
+def row_admissible_masks_mass(m: np.ndarray, tau: float, tie_eps: float = TIE_EPS) -> list:
+    """Every keep set a correct implementation may produce for a fragile row
+    of masses: prefix length k-1, k or k+1 of the descending-mass order, and
+    the tie band taken just inside or just outside tie_eps (the selection of
+    reading 2 with a decision moved across a threshold it lies within
+    FRAGILE_EPS of)."""
+    m = np.asarray(m, dtype=np.float64)
+    n = len(m)
+    base = select_row_mass(m, tau, tie_eps)
+    if tau >= 1.0:
+        return [base["keep"]]
+    order = np.lexsort((np.arange(n), -m))
+    out = []
+    for k in (base["k"] - 1, base["k"], base["k"] + 1):
+        if not 1 <= k <= n:
+            continue
+        for eps in (tie_eps - 2 * FRAGILE_EPS, tie_eps, tie_eps + 2 * FRAGILE_EPS):
+            keep = _keep_from_cut(m, order, k, eps)
+            if not any(np.array_equal(keep, o) for o in out):
+                out.append(keep)
+    return out
+
+
 def mask_from_mass(mass: np.ndarray, tau: float):
     """Block mask uint8 [B, H, nB, nB] from masses [B, H, nB, nB]; the report
     lists the fragile rows (a decision within FRAGILE_EPS of a threshold)."""

@@ -27,6 +27,10 @@ Readings (the paper is silent on these points):
    all-zero shape; d_size is +inf when exactly one area is 0, 0 when both are.
    d_shape is 0 for two empty shapes.
 3. The Clopper-Pearson upper bound at u = n is 1.
+
+Pins: ``ciede2000`` is pinned in its lightness and chroma terms by closed
+forms; its hue weighting (T, delta-theta, R_T, S_H) only by symmetry and
+hue-wrap continuity, so d_color is parity unpinned in those terms.
 """
 import math
 

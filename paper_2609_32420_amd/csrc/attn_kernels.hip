@@ -3,12 +3,13 @@
 // recomputed and only the key blocks listed for a query block are visited.
 //
 // One workgroup per query block (BS queries, BS/32 waves of 32 queries).  The
-// workgroup walks its compacted key-block list in stages of 32 keys.  K and V
-// stages are copied from HBM straight into LDS (global_load_lds, no register
-// staging) through a ring of four buffers, three stages ahead of the one being
-// computed, so a load has three stages of MFMA work to land.  S^T = K Q^T and
-// O^T += V^T P^T run on bf16 MFMA 32x32x16 with fp32 accumulation; the online
-// softmax runs in fp32 in the exp2 domain.
+// workgroup walks its compacted key-block list in stages of BS/2 keys (half a
+// key block).  K and V stages are copied from HBM straight into LDS
+// (global_load_lds, no register staging) into two slots each: the K tile of a
+// stage is issued two stages before its scores are computed, the V tile one
+// stage before its P.V product.  S^T = K Q^T and O^T += V^T P^T run on bf16
+// MFMA 32x32x16 with fp32 accumulation; the online softmax runs in fp32 in
+// the exp2 domain.
 //
 // Computing S^T (keys as MFMA rows, queries as columns) puts every score of a
 // query in one lane pair (lane q and lane q+32), so the row max is one
@@ -42,15 +43,16 @@ constexpr int kWaitVm0 = 0x0F70;
 // barrier are written as inline assembly.  Issued through the compiler
 // builtin, a direct load makes every later LDS read look like it may alias
 // the transfer, and the compiler then drains all outstanding loads
-// (vmcnt(0)) before each operand read, which removes the prefetch.  Nothing
-// else in this kernel uses M0.
+// (vmcnt(0)) before each operand read, which removes the prefetch.  The
+// asm writes M0 and declares it clobbered, so the compiler keeps no value of
+// its own in M0 across a load.
 //
 // 16 bytes per lane from base + voff to LDS offset lds_off + 16 * lane; base
 // and lds_off are the same in every lane.
 __device__ inline void dma16(const void *base, unsigned voff, unsigned lds_off) {
   asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(base),
                "s"(__builtin_amdgcn_readfirstlane(lds_off))
-               : "memory");
+               : "memory", "m0");
 }
 // Wait until every direct load and LDS read of this wave has completed, then
 // meet the other waves.

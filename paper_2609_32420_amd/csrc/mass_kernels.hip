@@ -21,6 +21,8 @@
 // contiguous bytes.
 #include "internal.h"
 
+#include <algorithm>
+
 namespace carnator {
 namespace {
 
@@ -96,13 +98,16 @@ struct MassCfg {
 
 template <int D, int BS>
 __global__ void __launch_bounds__(64 * kMassWaves)
-mass_pass_kernel(View q, View k, int H, int N, int nB, float c2, float2 *__restrict__ rec,
-                 float *__restrict__ lse2) {
+mass_pass_kernel(View q, View k, int H, int N, int nB, int bh0, float c2,
+                 float2 *__restrict__ rec, float *__restrict__ lse2) {
   using C = MassCfg<D, BS>;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
   const int ng = (nB + C::QPW - 1) / C::QPW;  // query groups per head
   const int qg = (int)(blockIdx.x % ng);
-  const int bh = (int)(blockIdx.x / ng);
+  // heads bh0 .. of the chunk this launch covers; records and log2-sum-exps
+  // are indexed inside the chunk
+  const int bc = (int)(blockIdx.x / ng);
+  const int bh = bh0 + bc;
   const int b = bh / H, h = bh - b * H;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -190,7 +195,7 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, float c2, float2 *__restr
       s0.m_run = s0.mb;                                                                  \
       s1.l_run = s1.l_run * __builtin_amdgcn_exp2f(s1.m_run == -INFINITY ? -INFINITY : s1.m_run - s1.mb) + t1; \
       s1.m_run = s1.mb;                                                                  \
-      float2 *rj = rec + ((int64_t)bh * nB + jj) * N;                                    \
+      float2 *rj = rec + ((int64_t)bc * nB + jj) * N;                                    \
       if (hh == 0 && qv0) rj[a0] = make_float2(s0.mb, t0);                               \
       if (hh == 0 && qv1) rj[a1] = make_float2(s1.mb, t1);                               \
     }                                                                                    \
@@ -208,8 +213,8 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, float c2, float2 *__restr
 #undef CARNATOR_MASS_STORE
 #undef CARNATOR_MASS_CHUNK_LOAD
 #undef CARNATOR_MASS_CHUNK_STORE
-  if (hh == 0 && qv0) lse2[(int64_t)bh * N + a0] = s0.m_run + log2f(s0.l_run);
-  if (hh == 0 && qv1) lse2[(int64_t)bh * N + a1] = s1.m_run + log2f(s1.l_run);
+  if (hh == 0 && qv0) lse2[(int64_t)bc * N + a0] = s0.m_run + log2f(s0.l_run);
+  if (hh == 0 && qv1) lse2[(int64_t)bc * N + a1] = s1.m_run + log2f(s1.l_run);
 }
 
 // One wave per (bh, i, j): M_ij = sum over the valid queries a of block i of
@@ -237,39 +242,61 @@ __global__ void __launch_bounds__(256) mass_reduce_kernel(const float2 *__restri
 
 }  // namespace
 
+// The records take 8 bytes per (query, key block) of a head: 67 MB at 32K
+// tokens, 887 MB at 119K.  Heads are processed in chunks whose records fit
+// in kMassScratchCap (at least one head per chunk), so the workspace stays
+// bounded whatever the number of heads.
+constexpr size_t kMassScratchCap = (size_t)4 << 30;
+
+static size_t mass_head_bytes(int N, int nB) {
+  return (size_t)nB * N * sizeof(float2) + (size_t)N * sizeof(float);
+}
+
+static int mass_chunk_heads(int BH, int N, int nB) {
+  const size_t per = mass_head_bytes(N, nB);
+  const size_t fit = kMassScratchCap / per;
+  return (int)std::max<size_t>(1, std::min<size_t>(fit, (size_t)BH));
+}
+
 size_t mass_scratch_bytes(int BH, int N, int nB) {
-  return align_up((size_t)BH * nB * N * sizeof(float2)) + align_up((size_t)BH * N * sizeof(float));
+  const int ch = mass_chunk_heads(BH, N, nB);
+  return align_up((size_t)ch * nB * N * sizeof(float2)) + align_up((size_t)ch * N * sizeof(float));
 }
 
 hipError_t launch_mass(View q, View k, int B, int H, int N, int d, int bs, float scale,
                        double *mass, void *scratch, hipStream_t s) {
   const int nB = (N + bs - 1) / bs;
   const int BH = B * H;
+  const int ch = mass_chunk_heads(BH, N, nB);
   float2 *rec = static_cast<float2 *>(scratch);
   float *lse2 = reinterpret_cast<float *>(static_cast<char *>(scratch) +
-                                          align_up((size_t)BH * nB * N * sizeof(float2)));
+                                          align_up((size_t)ch * nB * N * sizeof(float2)));
   const float c2 = scale * 1.4426950408889634f;
   const int qpw = kMassQueries / bs;
-  const dim3 grid((unsigned)(BH * ((nB + qpw - 1) / qpw)));
-  hipError_t e = hipSuccess;
-#define CARNATOR_MASS(DD, BB)                                                                   \
-  do {                                                                                          \
-    using C = MassCfg<DD, BB>;                                                                  \
-    e = hipFuncSetAttribute(reinterpret_cast<const void *>(&mass_pass_kernel<DD, BB>),          \
-                            hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);                \
-    if (e != hipSuccess) return e;                                                              \
+  for (int bh0 = 0; bh0 < BH; bh0 += ch) {
+    const int nh = std::min(ch, BH - bh0);
+    const dim3 grid((unsigned)(nh * ((nB + qpw - 1) / qpw)));
+    hipError_t e = hipSuccess;
+#define CARNATOR_MASS(DD, BB)                                                                    \
+  do {                                                                                           \
+    using C = MassCfg<DD, BB>;                                                                   \
+    e = hipFuncSetAttribute(reinterpret_cast<const void *>(&mass_pass_kernel<DD, BB>),           \
+                            hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);                 \
+    if (e != hipSuccess) return e;                                                               \
     hipLaunchKernelGGL((mass_pass_kernel<DD, BB>), grid, dim3(C::NT), C::LDS, s, q, k, H, N, nB, \
-                       c2, rec, lse2);                                                          \
+                       bh0, c2, rec, lse2);                                                      \
   } while (0)
-  if (d == 128 && bs == 128) CARNATOR_MASS(128, 128);
-  else if (d == 128 && bs == 64) CARNATOR_MASS(128, 64);
-  else if (d == 64 && bs == 128) CARNATOR_MASS(64, 128);
-  else CARNATOR_MASS(64, 64);
+    if (d == 128 && bs == 128) CARNATOR_MASS(128, 128);
+    else if (d == 128 && bs == 64) CARNATOR_MASS(128, 64);
+    else if (d == 64 && bs == 128) CARNATOR_MASS(64, 128);
+    else CARNATOR_MASS(64, 64);
 #undef CARNATOR_MASS
-  const int64_t total = (int64_t)BH * nB * nB;
-  hipLaunchKernelGGL(mass_reduce_kernel, dim3((unsigned)((total + 3) / 4)), dim3(256), 0, s, rec,
-                     lse2, N, nB, bs, total, mass);
-  return hipGetLastError();
+    const int64_t total = (int64_t)nh * nB * nB;
+    hipLaunchKernelGGL(mass_reduce_kernel, dim3((unsigned)((total + 3) / 4)), dim3(256), 0, s, rec,
+                       lse2, N, nB, bs, total, mass + (int64_t)bh0 * nB * nB);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace carnator

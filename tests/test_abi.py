@@ -257,6 +257,20 @@ def test_exact_mass_entry_points_reject(L):
     # one 8-byte record per (query, key block) and a 4-byte log-sum-exp per query
     big = _shape(1, 12, 32760, 128, 128)
     assert L.carnator_block_mass_exact_workspace_size(ctypes.byref(big)) >= 12 * 32760 * (256 * 8 + 4)
+    # heads in chunks whose records fit in 4 GiB: 4 of 24 heads at 119,056
+    # tokens (21 GB for all of them), one head beyond the cap at the largest N
+    cap = 4 << 30
+    per = 119056 * (931 * 8 + 4)
+    hv = _shape(1, 24, 119056, 128, 128)
+    need = L.carnator_block_mass_exact_workspace_size(ctypes.byref(hv))
+    assert 4 * per <= need <= cap and need < 5 * per
+    one = _shape(1, 3, 2048 * 128, 128, 128)
+    need1 = L.carnator_block_mass_exact_workspace_size(ctypes.byref(one))
+    assert 2048 * 128 * (2048 * 8 + 4) <= need1 < 2 * 2048 * 128 * (2048 * 8 + 4)
+    # a workspace one byte short of the chunked size is rejected before any launch
+    qv = _view(sn=128)
+    assert m(ctypes.byref(qv), ctypes.byref(qv), ctypes.byref(hv), 0.0, p, ws, need - 1, None) == -5
+    assert "workspace" in _err(L)
     sel = L.carnator_select_block_mask
     assert sel(None, ctypes.byref(s), 0.9, p, None, None) == -1
     assert sel(p, ctypes.byref(s), 0.9, None, None, None) == -1

@@ -285,7 +285,63 @@ def test_attention_tiny_workload_full():
     _compare_rows(o, ro, lse, rl, rows, wl.seq_len, wl.block)
 
 
-@pytest.mark.parametrize("wid", [1, 2, 3, 4])
+# The 32K and CogVideoX-shaped workloads in full: every query block of every
+# head, through the call and kernel the bench times (compacted lists, no LSE:
+# bsattn_kernel<128, 128, false> and <64, 128, false>), with the oracle run
+# one head at a time.  The heads are split over several tests so that each
+# stays well inside the per-test time limit; the GPU outputs are computed
+# once per workload.
+_FULL = {}
+
+
+def _full_workload(wid):
+    if wid not in _FULL:
+        _FULL.clear()
+        wl, x = _inputs(wid)
+        want_mask, _ = _oracle_mask(x, wl)
+        cols = None if x["col_flags"] is None else x["col_flags"].cpu().numpy()
+        merged = oracle.merge_target_rows(want_mask, x["row_flags"].cpu().numpy(), cols)
+        dm = torch.as_tensor(merged, device=DEV)
+        lists = P.compact_block_mask(dm)
+        o = P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists, wl.block)
+        o_lse, lse = P.block_sparse_attn(x["q"], x["k"], x["v"], dm, wl.block, return_lse=True)
+        torch.cuda.synchronize()
+        _say("merged density %.4f" % merged.mean())
+        _FULL[wid] = (wl, x, merged, o, o_lse, lse)
+    return _FULL[wid]
+
+
+@pytest.mark.parametrize("wid,part,parts", [(1, 0, 2), (1, 1, 2), (2, 0, 4), (2, 1, 4), (2, 2, 4), (2, 3, 4)])
+def test_attention_full_workload(wid, part, parts):
+    wl, x, merged, o, o_lse, lse = _full_workload(wid)
+    H, N, bs = wl.heads, wl.seq_len, wl.block
+    # the LSE kernel computes the same O bit for bit
+    assert torch.equal(o.view(torch.int16), o_lse.view(torch.int16))
+    og = o.float().cpu().numpy()
+    lg = lse.cpu().numpy().astype(np.float64)
+    worst = (0.0, -1)
+    dd = rr = 0.0
+    for h in range(part * H // parts, (part + 1) * H // parts):
+        ro, rl = oracle.block_sparse_attention(oracle.to_f64(x["q"][:, h:h + 1]), oracle.to_f64(x["k"][:, h:h + 1]),
+                                               oracle.to_f64(x["v"][:, h:h + 1]), merged[:, h:h + 1], bs)
+        d = og[:, h] - ro[:, 0]
+        mx = float(np.abs(d).max())
+        worst = max(worst, (mx, h))
+        dd += float((d * d).sum())
+        rr += float((ro * ro).sum())
+        assert mx <= ATOL, (h, mx)
+        hd = float(np.linalg.norm(d) / np.linalg.norm(ro))
+        assert hd <= REL_L2, (h, hd)
+        assert np.abs(lg[:, h] - rl[:, 0]).max() <= 1e-3
+    rel = math.sqrt(dd / rr)
+    _say("%s heads %d..%d of %d, all %d rows: worst head %d max|d| %.3e, relL2 %.3e" % (
+        wl.name, part * H // parts, (part + 1) * H // parts - 1, H, wl.n_blocks, worst[1], worst[0], rel))
+    assert rel <= REL_L2
+    if part == parts - 1:
+        _FULL.clear()
+
+
+@pytest.mark.parametrize("wid", [3, 4])
 def test_attention_sampled_rows(wid):
     wl, x = _inputs(wid)
     H = wl.heads
@@ -312,7 +368,7 @@ def test_attention_sampled_rows(wid):
     _compare_rows(o, o_ref, lse, l_ref, rows, wl.seq_len, wl.block)
 
 
-@pytest.mark.parametrize("wid", [0, 1])
+@pytest.mark.parametrize("wid", [0, 1, 2])
 def test_end_to_end_path(wid):
     """GPU builder -> GPU merge -> GPU attention against the oracle chain."""
     wl, x = _inputs(wid)
@@ -322,7 +378,8 @@ def test_end_to_end_path(wid):
     torch.cuda.synchronize()
     want_mask, fragile = _oracle_mask(x, wl)
     assert not fragile
-    merged = oracle.merge_target_rows(want_mask, x["row_flags"].cpu().numpy())
+    cols = None if x["col_flags"] is None else x["col_flags"].cpu().numpy()
+    merged = oracle.merge_target_rows(want_mask, x["row_flags"].cpu().numpy(), cols)
     np.testing.assert_array_equal(mask.cpu().numpy(), merged)
     rows = _sample_rows(wl, merged, x["row_flags"].cpu().numpy(), min(wl.heads, 2), n_random=8)
     ro, rl = oracle.block_sparse_attention(oracle.to_f64(x["q"][:, :2]), oracle.to_f64(x["k"][:, :2]),
@@ -331,7 +388,7 @@ def test_end_to_end_path(wid):
     _compare_rows(o, ro, None, None, [r for r in rows if r[1] < 2], wl.seq_len, wl.block)
 
 
-@pytest.mark.parametrize("wid", [0, 1])
+@pytest.mark.parametrize("wid", [0, 1, 2])
 def test_attention_from_lists_matches_mask_call(wid):
     """carnator_block_sparse_attn_lists on the lists of carnator_compact_block_mask
     runs the same kernel as carnator_block_sparse_attn: bit-identical O and LSE."""
@@ -356,10 +413,14 @@ def test_attention_ragged_shapes_and_dims(N, bs, d):
     m = synth.random_mask(2, 2, nb, 0.5, N)
     m[..., -1] = 1  # the partial tail block is visited by every row
     o, lse = P.block_sparse_attn(q, k, v, torch.as_tensor(m, device=DEV), bs, return_lse=True)
+    o_plain = P.block_sparse_attn(q, k, v, torch.as_tensor(m, device=DEV), bs)
     torch.cuda.synchronize()
     ro, rl = oracle.block_sparse_attention(oracle.to_f64(q), oracle.to_f64(k), oracle.to_f64(v), m, bs)
     rows = [(b, h, i) for b in range(2) for h in range(2) for i in range(nb)]
     _compare_rows(o, ro, lse, rl, rows, N, bs)
+    # the kernel without the LSE (its own code object for every (d, block))
+    _compare_rows(o_plain, ro, None, None, rows, N, bs)
+    assert torch.equal(o.view(torch.int16), o_plain.view(torch.int16))
 
 
 def test_attention_empty_rows_and_explicit_scale():

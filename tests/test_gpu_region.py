@@ -119,7 +119,7 @@ def test_compaction_region_bit_exact(nb, density, heads, p_act):
     np.testing.assert_array_equal(order.cpu().numpy(), word)
 
 
-@pytest.mark.parametrize("wid", [0, 1])
+@pytest.mark.parametrize("wid", [0, 1, 2])
 def test_region_restricted_attention(wid):
     """Historical mask -> bank slot -> regions from the evidence -> block flags
     -> restricted lists -> attention of the active rows only."""
@@ -134,7 +134,11 @@ def test_region_restricted_attention(wid):
     lse = torch.full((wl.batch, wl.heads, wl.seq_len), 7.0, dtype=torch.float32, device=DEV)
     o, lse = P.block_sparse_attn_lists(x["q"], x["k"], x["v"], (rp, ci, order), wl.block, out=sentinel,
                                        n_rows=n, return_lse=True, lse=lse)
+    # the kernel without the LSE writes the same rows, bit for bit
+    o_plain = P.block_sparse_attn_lists(x["q"], x["k"], x["v"], (rp, ci, order), wl.block,
+                                        out=torch.full_like(x["q"], 3.0), n_rows=n)
     torch.cuda.synchronize()
+    assert torch.equal(o.view(torch.int16), o_plain.view(torch.int16))
     nb = wl.n_blocks
     mask = oracle.unpack_mask(bits.cpu().numpy().view(np.uint64), nb)
     act_np, ctx_np = act.cpu().numpy(), ctx.cpu().numpy()

@@ -100,3 +100,27 @@ def test_selection_on_masses():
     # selection depends on the masses only through their ratios
     mk, _ = oracle.mask_from_mass(np.array([[[[0.2, 0.5, 0.3], [0.1, 0.1, 0.8], [1 / 3, 1 / 3, 1 / 3]]]]), 0.6)
     assert mk[0, 0].tolist() == [[0, 1, 1], [0, 0, 1], [1, 1, 0]]
+
+
+def test_admissible_masks_on_masses():
+    # the list holds the selection's mask and the prefixes one shorter and
+    # one longer (masses far from the tie band: no other variant)
+    m = np.array([0.2, 0.5, 0.3])
+    alts = [a.tolist() for a in oracle.row_admissible_masks_mass(m, 0.7)]
+    assert alts == [[False, True, False], [False, True, True], [True, True, True]]
+    # 0.5 + 0.25 reaches tau = 0.75 exactly (a fragile row): the prefixes of
+    # length 2 and 3 are both admissible, the selection's among them
+    m = np.array([0.25, 0.5, 0.25])
+    r = oracle.select_row_mass(m, 0.75)
+    assert r["fragile"]
+    alts = [a.tolist() for a in oracle.row_admissible_masks_mass(m, 0.75)]
+    assert r["keep"].tolist() in alts
+    assert [True, True, False] in alts and [True, True, True] in alts and [False, True, False] in alts
+    # a mass exactly 1e-6 below the cut mass: in the band or just outside it
+    t = np.array([0.3 - 1e-6, 0.3, 0.4 + 1e-6])
+    r = oracle.select_row_mass(t, 0.5)
+    assert r["fragile"] and r["k"] == 2
+    alts = [a.tolist() for a in oracle.row_admissible_masks_mass(t, 0.5)]
+    assert [True, False, True] in alts and [False, True, True] in alts
+    # tau >= 1 keeps everything, whatever the masses
+    assert [a.tolist() for a in oracle.row_admissible_masks_mass(m, 1.0)] == [[True, True, True]]
