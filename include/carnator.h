@@ -84,7 +84,7 @@
 extern "C" {
 #endif
 
-#define CARNATOR_ABI_VERSION 5
+#define CARNATOR_ABI_VERSION 6
 
 typedef enum {
   CARNATOR_OK = 0,
@@ -483,7 +483,8 @@ int carnator_block_sparse_attn_lists(const carnator_view *q, const carnator_view
  *   idx_out      int32 [nq, topk];  sim_out fp32 [nq, topk]
  *   all_sim_out  fp32 [nq, m] or NULL (every cosine)
  *   topk         1 .. min(m, 64)
- *   workspace    at least carnator_signature_sim_workspace_size(nq, m, topk) bytes
+ *   workspace    at least carnator_signature_sim_workspace_size(nq, m, topk)
+ *                bytes, 256-byte aligned (the fp64 cosines [nq, m])
  * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED (topk > 64), E_ALIGN, E_WORKSPACE, E_HIP.
  */
 size_t carnator_signature_sim_workspace_size(int64_t nq, int64_t m, int32_t topk);
@@ -491,6 +492,29 @@ int carnator_signature_sim(const float *query, int64_t nq, const float *bank, in
                            int64_t dim, int64_t ld, int32_t topk, int32_t *idx_out,
                            float *sim_out, float *all_sim_out, void *workspace,
                            size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * carnator_signature_sim without a workspace, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments (minus the workspace),
+ * same results and errors as carnator_signature_sim.
+ *
+ * The scratch (the fp64 cosines [nq, m]) is a library-owned device array of
+ * 4 MiB, one copy per GPU the library runs on, held until the process ends;
+ * its device address is looked up on the first call on each device.  The
+ * call allocates nothing (no hipMalloc, no hipFree, no allocating library
+ * routine).  Limit: nq * m <= 524,288 cosines (e.g. 128 queries against
+ * 4,096 rows, or one query against 524,288 rows); beyond it the call returns
+ * E_WORKSPACE and enqueues nothing.  Every cosine is written before it is
+ * read, so nothing needs clearing between calls.  Every call on one GPU
+ * shares that GPU's scratch: calls that overlap on one GPU (other streams,
+ * other host threads) RACE and must be serialised by the caller.
+ * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED (topk > 64), E_ALIGN, E_WORKSPACE
+ * (nq * m above the limit), E_HIP.
+ */
+int carnator_signature_sim_noalloc(const float *query, int64_t nq, const float *bank, int64_t m,
+                                   int64_t dim, int64_t ld, int32_t topk, int32_t *idx_out,
+                                   float *sim_out, float *all_sim_out, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libcarnator.so")
 
 CARNATOR_OK = 0
 # CARNATOR_ABI_VERSION of include/carnator.h this binding marshals for
-ABI_VERSION = 5
+ABI_VERSION = 6
 STATUS = {0: "OK", -1: "E_NULL", -2: "E_SHAPE", -3: "E_UNSUPPORTED", -4: "E_ALIGN",
           -5: "E_WORKSPACE", -6: "E_HIP"}
 
@@ -37,7 +37,7 @@ EXPORTS = (
     "carnator_block_sparse_attn_rows",
     "carnator_block_sparse_attn_workspace_size", "carnator_block_sparse_attn",
     "carnator_block_sparse_attn_lists",
-    "carnator_signature_sim_workspace_size", "carnator_signature_sim",
+    "carnator_signature_sim_workspace_size", "carnator_signature_sim", "carnator_signature_sim_noalloc",
     "carnator_ciede2000", "carnator_shape_descriptor", "carnator_object_discrepancy", "carnator_compat_gate",
     "carnator_clopper_pearson_upper",
 )
@@ -103,6 +103,7 @@ def lib() -> ctypes.CDLL:
                                                                 P, P]),
             "carnator_signature_sim_workspace_size": (SZ, [I64, I64, I32]),
             "carnator_signature_sim": (ctypes.c_int, [P, I64, P, I64, I64, I64, I32, P, P, P, P, SZ, P]),
+            "carnator_signature_sim_noalloc": (ctypes.c_int, [P, I64, P, I64, I64, I64, I32, P, P, P, P]),
             "carnator_ciede2000": (ctypes.c_int, [P, P, I64, P]),
             "carnator_shape_descriptor": (ctypes.c_int, [P, I32, I32, I32, P, P]),
             "carnator_object_discrepancy": (ctypes.c_int, [F64, F64, P, P, I32, P, P, P]),
@@ -615,6 +616,31 @@ def signature_sim(query: torch.Tensor, bank: torch.Tensor, topk: int, return_all
         workspace = signature_sim_workspace(nq, m, topk, dev)
     _check(L.carnator_signature_sim(_ptr(query), nq, _ptr(bank), m, dim, bank.stride(0), int(topk), _ptr(idx),
                                     _ptr(sim), _ptr(allsim), _ptr(workspace), workspace.numel(), _stream(query)))
+    return (idx, sim, allsim) if return_all else (idx, sim)
+
+
+def signature_sim_noalloc(query: torch.Tensor, bank: torch.Tensor, topk: int, return_all: bool = False,
+                          out=None):
+    """signature_sim on the library's own scratch (carnator_signature_sim_noalloc):
+    no workspace is allocated by the call.  ``out`` may pass preallocated
+    (idx, sim) so that the call allocates nothing at all."""
+    if query.dim() == 1:
+        query = query[None]
+    if query.dtype != torch.float32 or bank.dtype != torch.float32 or bank.dim() != 2:
+        raise ValueError("query [nq, D] and bank [M, ld] must be fp32")
+    if not query.is_contiguous() or bank.stride(1) != 1:
+        raise ValueError("query must be contiguous and bank rows contiguous")
+    nq, dim = query.shape
+    m = bank.shape[0]
+    dev = query.device
+    if out is not None:
+        idx, sim = out
+    else:
+        idx = torch.empty(nq, topk, dtype=torch.int32, device=dev)
+        sim = torch.empty(nq, topk, dtype=torch.float32, device=dev)
+    allsim = torch.empty(nq, m, dtype=torch.float32, device=dev) if return_all else None
+    _check(lib().carnator_signature_sim_noalloc(_ptr(query), nq, _ptr(bank), m, dim, bank.stride(0), int(topk),
+                                                _ptr(idx), _ptr(sim), _ptr(allsim), _stream(query)))
     return (idx, sim, allsim) if return_all else (idx, sim)
 
 

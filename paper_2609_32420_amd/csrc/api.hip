@@ -505,17 +505,16 @@ int carnator_block_sparse_attn_rows(const carnator_view *q, const carnator_view 
 
 // ---------------------------------------------------------------- signature scan
 
+// Signature workspace: the fp64 cosines [nq][m].
 size_t carnator_signature_sim_workspace_size(int64_t nq, int64_t m, int32_t topk) {
   (void)topk;
   if (nq < 1 || m < 1) return 0;
   return align_up((size_t)nq * m * 8);
 }
 
-int carnator_signature_sim(const float *query, int64_t nq, const float *bank, int64_t m,
-                           int64_t dim, int64_t ld, int32_t topk, int32_t *idx_out,
-                           float *sim_out, float *all_sim_out, void *workspace, size_t ws_bytes,
-                           hipStream_t stream) {
-  int rc;
+static int check_signature(const float *query, int64_t nq, const float *bank, int64_t m,
+                           int64_t dim, int64_t ld, int32_t topk, const int32_t *idx_out,
+                           const float *sim_out) {
   if (!query || !bank || !idx_out || !sim_out)
     return fail(CARNATOR_E_NULL, "query, bank, idx_out and sim_out must be non-NULL");
   if (nq < 1 || m < 1 || dim < 1 || ld < dim)
@@ -525,12 +524,44 @@ int carnator_signature_sim(const float *query, int64_t nq, const float *bank, in
   if (topk > 64) return fail(CARNATOR_E_UNSUPPORTED, "topk must be <= 64");
   if (dim % 4 || ld % 4 || reinterpret_cast<uintptr_t>(query) % 16 || reinterpret_cast<uintptr_t>(bank) % 16)
     return fail(CARNATOR_E_ALIGN, "dim and ld must be multiples of 4 and query/bank 16-byte aligned");
+  return CARNATOR_OK;
+}
+
+int carnator_signature_sim(const float *query, int64_t nq, const float *bank, int64_t m,
+                           int64_t dim, int64_t ld, int32_t topk, int32_t *idx_out,
+                           float *sim_out, float *all_sim_out, void *workspace, size_t ws_bytes,
+                           hipStream_t stream) {
+  int rc;
+  if ((rc = check_signature(query, nq, bank, m, dim, ld, topk, idx_out, sim_out))) return rc;
   const size_t need = carnator_signature_sim_workspace_size(nq, m, topk);
   if ((rc = check_ws(workspace, ws_bytes, need))) return rc;
   double *sims = static_cast<double *>(workspace);
   hipError_t e = launch_sig(query, nq, bank, m, dim, ld, topk, idx_out, sim_out, all_sim_out, sims,
                             stream);
   if (e != hipSuccess) return hip_fail(e, "signature_sim");
+  return ok();
+}
+
+// The same call on the library's own scratch: no workspace argument and no
+// allocation of any kind.
+int carnator_signature_sim_noalloc(const float *query, int64_t nq, const float *bank, int64_t m,
+                                   int64_t dim, int64_t ld, int32_t topk, int32_t *idx_out,
+                                   float *sim_out, float *all_sim_out, hipStream_t stream) {
+  int rc;
+  if ((rc = check_signature(query, nq, bank, m, dim, ld, topk, idx_out, sim_out))) return rc;
+  const size_t need = carnator_signature_sim_workspace_size(nq, m, topk);
+  if (need > kSigStaticScratchBytes)
+    return fail(CARNATOR_E_WORKSPACE,
+                "nq * m = %lld cosines need %zu bytes of scratch; the no-allocation call holds %zu "
+                "(nq * m <= %zu)",
+                (long long)(nq * m), need, kSigStaticScratchBytes,
+                kSigStaticScratchBytes / sizeof(double));
+  void *base = nullptr;
+  hipError_t e = sig_static_scratch(&base);
+  if (e != hipSuccess) return hip_fail(e, "signature_sim_noalloc: scratch address");
+  e = launch_sig(query, nq, bank, m, dim, ld, topk, idx_out, sim_out, all_sim_out,
+                 static_cast<double *>(base), stream);
+  if (e != hipSuccess) return hip_fail(e, "signature_sim_noalloc");
   return ok();
 }
 

@@ -163,8 +163,14 @@ hipError_t launch_bsattn(View q, View k, View v, uint16_t *out, int64_t osb, int
                          float scale, float *lse, hipStream_t s);
 
 // ---- signature scan ----------------------------------------------------------
+// sims: fp64 [nq][m] scratch.
 hipError_t launch_sig(const float *query, int64_t nq, const float *bank, int64_t m, int64_t dim,
                       int64_t ld, int topk, int32_t *idx, float *sim, float *all_sim,
                       double *sims, hipStream_t s);
+// The library-owned scratch of the no-allocation signature call (fp64
+// cosines): the device address of this GPU's copy (the current device),
+// looked up once per device.
+constexpr size_t kSigStaticScratchBytes = (size_t)4 << 20;
+hipError_t sig_static_scratch(void **ptr);
 
 }  // namespace carnator

@@ -11,6 +11,14 @@
 
 #include <math.h>
 
+#include <mutex>
+
+// Scratch of the no-allocation entry point (carnator_signature_sim_noalloc):
+// the fp64 cosines.  Each GPU the library runs on holds one copy until the
+// process ends.  Host code never uses this name as an address: it asks the
+// runtime for the array's device address (once per device).
+static __device__ __align__(256) unsigned char scratch[carnator::kSigStaticScratchBytes];
+
 namespace carnator {
 namespace {
 
@@ -496,6 +504,25 @@ hipError_t launch_staged(const float *query, int64_t q0, const float *bank, int6
 }
 
 }  // namespace
+
+hipError_t sig_static_scratch(void **ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_sig(const float *query, int64_t nq, const float *bank, int64_t m, int64_t dim,
                       int64_t ld, int topk, int32_t *idx, float *sim, float *all_sim,

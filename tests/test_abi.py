@@ -161,6 +161,16 @@ def test_merge_compact_signature_reject(L):
     assert sig(q, 1, q, 8, 16, 8, 2, q, q, None, q, 1 << 20, None) == -2
     assert sig(q, 1, q, 8, 18, 20, 2, q, q, None, q, 1 << 20, None) == -4
     assert sig(q, 1, q, 8, 16, 16, 2, q, q, None, q, 8, None) == -5
+    assert L.carnator_signature_sim_workspace_size(2, 4096, 8) == 2 * 4096 * 8
+    # the no-allocation call: same checks, and nq * m bounded by its 4 MiB scratch
+    na = L.carnator_signature_sim_noalloc
+    assert na(None, 1, q, 8, 16, 16, 2, q, q, None, None) == -1
+    assert na(q, 1, q, 8, 16, 16, 9, q, q, None, None) == -2
+    assert na(q, 1, q, 100, 16, 16, 65, q, q, None, None) == -3
+    assert na(q, 1, q, 8, 18, 20, 2, q, q, None, None) == -4
+    assert na(q, 1, q, 524289, 16, 16, 2, q, q, None, None) == -5
+    assert na(q, 2, q, 262145, 16, 16, 2, q, q, None, None) == -5
+    assert "524288" in _err(L)
 
 
 def test_python_binding_raises_without_gpu_tensors():
