@@ -232,6 +232,68 @@ def exact_mass_pass(P, torch, stream, sets, wl, steps):
     }
 
 
+def workload_pass(P, torch, stream, wids, steps):
+    """The other workload shapes of the paper's backbones (CogVideoX-5B 17.8K
+    tokens at d = 64, Wan2.1-14B 75.6K, HunyuanVideo 119K), measured in the
+    same run after the timed region: one input set each (its historical Q/K
+    alone exceed the 256 MB Infinity Cache, so the builder reads HBM), every
+    call timed alone between two events, the attention from the lists (the
+    kernel the headline times) against the bf16 peak on executed FLOPs."""
+    import synth
+    out = {}
+    dev = torch.device("cuda:0")
+    for wid in wids:
+        wl = synth.WORKLOADS[wid]
+        B, H, N, d, bs, nb = wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block, wl.n_blocks
+        print("bench: workload %s" % wl.name, file=sys.stderr, flush=True)
+        x = synth.attention_inputs(wl, seed=0, device=dev)
+        mask = torch.empty(B, H, nb, nb, dtype=torch.uint8, device=dev)
+        ws_mask = P.build_block_mask_workspace(x["q_hist"], bs)
+        ws_cmp = P.compact_block_mask_workspace(mask)
+        R = B * H * nb
+        lists = (torch.empty(R + 1, dtype=torch.int32, device=dev), torch.empty(R * nb, dtype=torch.int32, device=dev),
+                 torch.empty(R, dtype=torch.int32, device=dev))
+        o = torch.empty_like(x["q"])
+        rows = x["row_flags"].contiguous()
+        cols = None if x["col_flags"] is None else x["col_flags"].contiguous()
+        t = {k: [] for k in ("build", "merge", "compact", "attn")}
+        for i in range(steps + 1):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(8)]
+            e[0].record(stream)
+            P.build_block_mask(x["q_hist"], x["k_hist"], bs, wl.tau, out=mask, workspace=ws_mask)
+            e[1].record(stream)
+            e[2].record(stream)
+            P.merge_target_rows(mask, rows, cols)
+            e[3].record(stream)
+            e[4].record(stream)
+            P.compact_block_mask(mask, trim=False, out=lists, workspace=ws_cmp)
+            e[5].record(stream)
+            e[6].record(stream)
+            P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists, bs, out=o)
+            e[7].record(stream)
+            if i > 0:
+                for k_, (a_, b_) in zip(("build", "merge", "compact", "attn"), ((0, 1), (2, 3), (4, 5), (6, 7))):
+                    t[k_].append((e[a_], e[b_]))
+        torch.cuda.synchronize()
+        ms = {k: float(np.median([a.elapsed_time(b) for a, b in v])) for k, v in t.items()}
+        fl = executed_flops(mask.cpu().numpy(), N, bs, d)
+        tf = fl / (ms["attn"] * 1e-3) / 1e12
+        bbytes = 2.0 * B * H * N * d * 2 + B * H * nb * nb
+        out[wl.name] = {
+            "heads": H, "seq_len": N, "head_dim": d, "block": bs, "mask_density": round(float(mask.float().mean().item()), 4),
+            "attn_ms_per_call": round(ms["attn"], 4), "attn_executed_tflop": round(fl / 1e12, 4),
+            "attn_executed_tflops": round(tf, 2), "attn_frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+            "attn_dense_equiv_tflops": round(dense_flops(B, H, N, d) / (ms["attn"] * 1e-3) / 1e12, 2),
+            "builder_ms_per_call": round(ms["build"], 4), "builder_GBps": round(bbytes / (ms["build"] * 1e-3) / 1e9, 1),
+            "builder_pct_hbm_peak": round(100.0 * bbytes / (ms["build"] * 1e-3) / 1e9 / PEAK_HBM_GBPS, 2),
+            "merge_ms_per_call": round(ms["merge"], 4), "compact_ms_per_call": round(ms["compact"], 4),
+            "timing": "median of %d calls, each alone between two events" % steps,
+        }
+        del x, mask, ws_mask, ws_cmp, lists, o
+        torch.cuda.empty_cache()
+    return out
+
+
 def ctypes_shape(P, wl):
     import ctypes
     return ctypes.byref(P.Shape(wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block))
@@ -331,6 +393,8 @@ def main():
     ap.add_argument("--no-bank", action="store_true", help="skip the bit-packed mask bank pass")
     ap.add_argument("--no-region", action="store_true", help="skip the region-restricted pass")
     ap.add_argument("--no-exact", action="store_true", help="skip the exact-mass builder pass")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the pass over the 17.8K, 75.6K and 119K-token workload shapes")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before timing, copy a buffer of this size once (a reference kernel of known "
                          "traffic for hardware byte counters)")
@@ -506,6 +570,10 @@ def main():
         res["region_restricted"] = region
     if exact is not None:
         res["exact_mass"] = exact
+    if not args.no_workloads:
+        del sets, masks, outs, lists
+        torch.cuda.empty_cache()
+        res["workloads"] = workload_pass(P, torch, stream, [w for w in (2, 3, 4) if w != args.workload], 5)
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(wl)
