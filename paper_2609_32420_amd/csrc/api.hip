@@ -98,7 +98,7 @@ AttnWs attn_layout(const carnator_shape *s) {
   w.order = off;
   off += align_up((size_t)R * 4);
   w.scratch = off;
-  off += compact_scratch_bytes(R);
+  off += compact_scratch_bytes(R, (int)nB);
   w.total = off;
   return w;
 }
@@ -256,7 +256,7 @@ int carnator_merge_target_rows(uint8_t *mask, const carnator_shape *s, const uin
 
 size_t carnator_compact_block_mask_workspace_size(const carnator_shape *s) {
   if (check_shape(s) != CARNATOR_OK) return 0;
-  return compact_scratch_bytes((int64_t)s->batch * s->heads * n_blocks(s));
+  return compact_scratch_bytes((int64_t)s->batch * s->heads * n_blocks(s), n_blocks(s));
 }
 
 int carnator_compact_block_mask(const uint8_t *mask, const carnator_shape *s, int32_t *row_ptr,

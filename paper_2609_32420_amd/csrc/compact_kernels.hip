@@ -382,6 +382,140 @@ __global__ void __launch_bounds__(kScanThreads) count_sort_kernel(const int32_t 
   }
 }
 
+// ---- the same row_ptr and order by several workgroups (chunks of kChunk rows)
+//
+//   sort_hist_kernel, one workgroup per chunk g: the chunk's key histogram
+//     (key = nB - length, nB + 1 for a left-out row) to hist[g K + key],
+//     K = nB + 2, and its length sum to csum[g];
+//   sort_scan_kernel, one workgroup: for each key, the exclusive prefix of
+//     its counts over the chunks plus the exclusive prefix of the key totals
+//     (key order) -- the first slot of chunk g's rows of each key -- and the
+//     exclusive scan of csum;
+//   sort_place_kernel, one workgroup per chunk: row_ptr of its rows (chunk
+//     offset plus a block scan), and each row's slot in order: its chunk's
+//     first slot for its key, plus the rows of that key in earlier waves of
+//     the chunk (per-wave counts, scanned per key), plus the lanes below it
+//     in its wave holding the same key (one ballot per key bit).
+// Within a chunk wave w holds rows 64 w .. 64 w + 63 in row order, so rows
+// of equal key keep their row order: the order the oracle defines.
+constexpr int kChunk = 1024;
+
+__device__ inline int sort_key(int L, int nB) { return L < 0 ? nB + 1 : nB - L; }
+
+__global__ void __launch_bounds__(kScanThreads) sort_hist_kernel(const int32_t *__restrict__ len,
+                                                                 int R, int nB, int G,
+                                                                 int32_t *__restrict__ hist,
+                                                                 int32_t *__restrict__ csum) {
+  extern __shared__ int hk[];  // nB + 2 counters
+  __shared__ int sh[kScanThreads / 64];
+  const int g = blockIdx.x, t = threadIdx.x;
+  for (int k = t; k < nB + 2; k += kScanThreads) hk[k] = 0;
+  __syncthreads();
+  const int r = g * kChunk + t;
+  const int L = r < R ? len[r] : 0;
+  if (r < R) atomicAdd(&hk[sort_key(L, nB)], 1);
+  int total;
+  (void)block_excl_scan(max(L, 0), sh, &total);
+  for (int k = t; k < nB + 2; k += kScanThreads) hist[(int64_t)g * (nB + 2) + k] = hk[k];
+  if (t == 0) csum[g] = total;
+}
+
+// One workgroup, thread t owning keys t, t + 1024, t + 2048: the chunk
+// prefix of each of its keys (G coalesced loads and stores per key, eight
+// loads in flight), then the key totals scanned in key order one pass of
+// 1024 keys at a time and added back; the chunk offsets of row_ptr, row_ptr[R]
+// and the number of rows not left out (the first slot of key nB + 1).
+__global__ void __launch_bounds__(kScanThreads) sort_scan_kernel(int R, int nB, int G,
+                                                                 int32_t *__restrict__ hist,
+                                                                 int32_t *__restrict__ csum,
+                                                                 int32_t *__restrict__ row_ptr,
+                                                                 int32_t *__restrict__ n_active) {
+  __shared__ int sh[kScanThreads / 64];
+  const int t = threadIdx.x;
+  const int K = nB + 2;
+  int carry = 0;
+  for (int k0 = 0; k0 < K; k0 += kScanThreads) {
+    const int k = k0 + t;
+    int tot = 0;
+    if (k < K) {
+      for (int g0 = 0; g0 < G; g0 += 8) {
+        int v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = g0 + u < G ? hist[(int64_t)(g0 + u) * K + k] : 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (g0 + u < G) hist[(int64_t)(g0 + u) * K + k] = tot;
+          tot += v[u];
+        }
+      }
+    }
+    int all;
+    const int ex = block_excl_scan(tot, sh, &all) + carry;
+    carry += all;
+    if (k < K) {
+      for (int g = 0; g < G; ++g) hist[(int64_t)g * K + k] += ex;
+    }
+  }
+  // chunk offsets of row_ptr
+  int rcarry = 0;
+  for (int g0 = 0; g0 < G; g0 += kScanThreads) {
+    const int g = g0 + t;
+    const int v = g < G ? csum[g] : 0;
+    int tot;
+    const int ex = block_excl_scan(v, sh, &tot);
+    if (g < G) csum[g] = rcarry + ex;
+    rcarry += tot;
+  }
+  if (t == 0) row_ptr[R] = rcarry;
+  // the first slot of key nB + 1 (chunk 0): written by the thread owning it
+  if (n_active != nullptr && t == (nB + 1) % kScanThreads) {
+    __threadfence_block();
+    *n_active = hist[nB + 1];
+  }
+}
+
+__global__ void __launch_bounds__(kScanThreads) sort_place_kernel(const int32_t *__restrict__ len,
+                                                                  int R, int nB, int G,
+                                                                  const int32_t *__restrict__ base,
+                                                                  const int32_t *__restrict__ coff,
+                                                                  int32_t *__restrict__ row_ptr,
+                                                                  int32_t *__restrict__ order) {
+  constexpr int kWaves = kScanThreads / 64;
+  extern __shared__ int wc[];  // (nB + 2) * kWaves per-wave counts, then slots
+  __shared__ int sh[kWaves];
+  const int g = blockIdx.x, t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int K = nB + 2;
+  for (int i = t; i < K * kWaves; i += kScanThreads) wc[i] = 0;
+  __syncthreads();
+  const int r = g * kChunk + t;
+  const bool on = r < R;
+  const int L = on ? len[r] : 0;
+  const int key = on ? sort_key(L, nB) : 0;
+  if (on) atomicAdd(&wc[key * kWaves + w], 1);
+  int total;
+  const int ex = block_excl_scan(on ? max(L, 0) : 0, sh, &total);  // ends with a barrier
+  if (on) row_ptr[r] = coff[g] + ex;
+  for (int k = t; k < K; k += kScanThreads) {
+    int run = base[(int64_t)g * K + k];
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) {
+      const int c = wc[k * kWaves + q];
+      wc[k * kWaves + q] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+  int kbits = 0;
+  while ((1 << kbits) <= nB + 1) ++kbits;
+  unsigned long long m = __ballot(on);
+  for (int b = 0; b < kbits; ++b) {
+    const unsigned long long ones = __ballot(on && ((key >> b) & 1));
+    m &= ((key >> b) & 1) ? ones : ~ones;
+  }
+  if (on) order[wc[key * kWaves + w] + __popcll(m & ((1ull << lane) - 1ull))] = r;
+}
+
 }  // namespace
 
 hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows,
@@ -392,11 +526,41 @@ hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows
   return hipGetLastError();
 }
 
-size_t compact_scratch_bytes(int64_t R) { return align_up((size_t)R * sizeof(int32_t)); }
+static int sort_chunks(int64_t R) { return (int)((R + kChunk - 1) / kChunk); }
 
-// row_ptr and order from the list lengths (one workgroup).
+// Lengths, then the chunk histograms and offsets of the multi-workgroup sort.
+size_t compact_scratch_bytes(int64_t R, int nB) {
+  const int G = sort_chunks(R);
+  return align_up((size_t)R * sizeof(int32_t)) + align_up((size_t)(nB + 2) * G * sizeof(int32_t)) +
+         align_up((size_t)G * sizeof(int32_t));
+}
+
+// Rows up to which the single-workgroup counting sort runs (one launch);
+// beyond, the chunked sort (three launches) spreads the walk over the CUs.
+constexpr int64_t kSingleSortRows = 4096;
+
+// row_ptr and order from the list lengths; sort_scratch: the histogram and
+// chunk offsets of compact_scratch_bytes.
 static hipError_t launch_sort(const int32_t *len, int64_t R, int nB, int32_t *row_ptr, int32_t *order,
-                              int32_t *n_active, hipStream_t s) {
+                              int32_t *n_active, void *sort_scratch, hipStream_t s) {
+  if (R > kSingleSortRows) {
+    const int G = sort_chunks(R);
+    int32_t *hist = static_cast<int32_t *>(sort_scratch);
+    int32_t *csum = reinterpret_cast<int32_t *>(static_cast<char *>(sort_scratch) +
+                                                align_up((size_t)(nB + 2) * G * sizeof(int32_t)));
+    const size_t hl = (size_t)(nB + 2) * sizeof(int32_t);
+    const size_t pl = (size_t)(nB + 2) * (kScanThreads / 64) * sizeof(int32_t);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sort_place_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(sort_hist_kernel, dim3((unsigned)G), dim3(kScanThreads), hl, s, len, (int)R, nB,
+                       G, hist, csum);
+    hipLaunchKernelGGL(sort_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, (int)R, nB, G, hist, csum,
+                       row_ptr, n_active);
+    hipLaunchKernelGGL(sort_place_kernel, dim3((unsigned)G), dim3(kScanThreads), pl, s, len, (int)R, nB,
+                       G, hist, csum, row_ptr, order);
+    return hipGetLastError();
+  }
   const size_t cnt_lds = (size_t)(nB + 2) * (kScanThreads / 64) * sizeof(uint32_t);
   const size_t len_lds = (size_t)R * sizeof(int16_t);
   hipError_t e;
@@ -429,7 +593,8 @@ hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_p
     else hipLaunchKernelGGL(KERNEL<32>, dim3(g), dim3(256), 0, s, __VA_ARGS__);          \
   } while (0)
   CARNATOR_ROWS(count_kernel, mask, R, nB, len);
-  hipError_t e = launch_sort(len, R, nB, row_ptr, order, nullptr, s);
+  hipError_t e = launch_sort(len, R, nB, row_ptr, order, nullptr,
+                             static_cast<char *>(scratch) + align_up((size_t)R * sizeof(int32_t)), s);
   if (e != hipSuccess) return e;
   CARNATOR_ROWS(fill_kernel, mask, R, nB, row_ptr, col_idx);
   return hipGetLastError();
@@ -458,7 +623,7 @@ hipError_t launch_fill_ones_bits(uint64_t *bits, int64_t R, int nB, hipStream_t 
 }
 
 size_t compact_bits_scratch_bytes(int64_t R, int B, int nB) {
-  return compact_scratch_bytes(R) + align_up((size_t)B * ((nB + 63) / 64) * sizeof(uint64_t));
+  return compact_scratch_bytes(R, nB) + align_up((size_t)B * ((nB + 63) / 64) * sizeof(uint64_t));
 }
 
 hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const uint8_t *rows,
@@ -471,7 +636,7 @@ hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const
   hipError_t e;
   if (cols != nullptr) {
     // the column flags of each batch entry, packed once like a mask row
-    colw = reinterpret_cast<uint64_t *>(static_cast<char *>(scratch) + compact_scratch_bytes(R));
+    colw = reinterpret_cast<uint64_t *>(static_cast<char *>(scratch) + compact_scratch_bytes(R, nB));
     if ((e = launch_pack(cols, B, nB, colw, s)) != hipSuccess) return e;
   }
   const int nw = (nB + 63) / 64;  // nB <= 2048
@@ -489,7 +654,10 @@ hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const
 #undef CARNATOR_G
     default: return hipErrorInvalidValue;
   }
-  if ((e = launch_sort(len, R, nB, row_ptr, order, n_active, s)) != hipSuccess) return e;
+  if ((e = launch_sort(len, R, nB, row_ptr, order, n_active,
+                       static_cast<char *>(scratch) + align_up((size_t)R * sizeof(int32_t)), s)) !=
+      hipSuccess)
+    return e;
   hipLaunchKernelGGL(fill_bits_kernel, dim3((unsigned)((R + 3) / 4)), dim3(256), 0, s, bits,
                      (int)R, nB, HnB, rows, colw, narrow, row_ptr, col_idx);
   return hipGetLastError();

@@ -109,8 +109,8 @@ hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows
                         const uint8_t *cols, hipStream_t s);
 
 // ---- compaction ------------------------------------------------------------
-// Scratch needed by launch_compact, in bytes.
-size_t compact_scratch_bytes(int64_t R);
+// Scratch needed by launch_compact, in bytes (R rows of nB key blocks).
+size_t compact_scratch_bytes(int64_t R, int nB);
 hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_ptr,
                           int32_t *col_idx, int32_t *order, void *scratch, hipStream_t s);
 

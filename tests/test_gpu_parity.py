@@ -155,11 +155,12 @@ def test_merge_bit_exact(wid):
     np.testing.assert_array_equal(got, oracle.merge_target_rows(m, rows, cols))
 
 
-# R = heads * nb rows.  The sort keeps its counters in LDS and the row lengths
-# beside them while 64 (nb + 1) + 2 R bytes fit in 152 KiB: (2048, 7) reads
-# the lengths from memory instead.
+# R = heads * nb rows.  Up to 4096 rows one workgroup sorts them (counters in
+# LDS, the row lengths beside them while they fit); beyond, chunks of 1024
+# rows are sorted by several workgroups: (931, 5), (2048, *) and the
+# 119K-token shape (931, 24: 22 chunks, the last partial).
 @pytest.mark.parametrize("nb,density,heads", [(3, 0.5, 5), (139, 0.3, 5), (256, 0.2, 5), (931, 0.1, 5),
-                                              (2048, 0.05, 5), (2048, 0.05, 7),
+                                              (2048, 0.05, 5), (2048, 0.05, 7), (931, 0.1, 24),
                                               # every row full but one: one length group in row order
                                               (64, 1.0, 3)])
 def test_compaction_bit_exact(nb, density, heads):

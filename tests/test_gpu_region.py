@@ -102,7 +102,8 @@ def test_region_block_flags(wid):
 # list; (2048, 7) keeps the sort's lengths in memory
 @pytest.mark.parametrize("nb,density,heads,p_act", [(3, 0.5, 5, 0.5), (7, 0.6, 3, 0.4), (63, 0.3, 3, 0.3),
                                                     (139, 0.3, 5, 0.2), (256, 0.2, 4, 0.15), (591, 0.1, 2, 0.2),
-                                                    (2048, 0.05, 7, 0.1), (100, 1.0, 2, 0.5), (50, 0.4, 2, 0.0),
+                                                    (2048, 0.05, 7, 0.1), (931, 0.1, 12, 0.2), (100, 1.0, 2, 0.5),
+                                                    (50, 0.4, 2, 0.0),
                                                     (50, 0.4, 2, 1.0)])
 def test_compaction_region_bit_exact(nb, density, heads, p_act):
     B = 2
