@@ -135,7 +135,8 @@ hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const
 // ---- region-restricted reuse -------------------------------------------------
 // Region codes (3 evidence, 2 band, 1 context, 0 outside) and the blend
 // weight W over [B][T][H][W] tokens from the evidence; scratch of
-// region_scratch_bytes; LDS of region_frame_lds per frame.
+// region_scratch_bytes; a frame must fit region_frame_lds bytes of LDS (a
+// workgroup stages a band of its rows with the rows within reach).
 size_t region_frame_lds(int H, int W);
 size_t region_scratch_bytes(int B, int T, int H, int W);
 hipError_t launch_regions(const uint8_t *evidence, int B, int T, int H, int W, int ra, int rc,

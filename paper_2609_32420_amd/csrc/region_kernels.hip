@@ -23,27 +23,35 @@
 namespace carnator {
 namespace {
 
-constexpr int kRegionThreads = 1024;
+constexpr int kRegionThreads = 256;
 
-// One workgroup of 1024 threads per (b, t) frame (few frames, each thread a
-// handful of tokens), the frame's evidence and row distances in LDS
-// (2 H W bytes).  Writes the region code (3 evidence, 2 band, 1 context,
-// 0 outside) and the capped distance of every token, and the largest band
-// distance of the frame (0 when it has no band).
+// One workgroup of 256 threads per band of BR rows of a (b, t) frame (grid
+// x the frame, y the band: at most 512 bands, any number of frames), so a
+// frame's rows spread over several CUs (a frame per workgroup left most of
+// the chip idle: 21 frames at 32K tokens).  The band's rows and the R =
+// r_active + r_context rows on either side that its distances can reach
+// (clipped at the frame border) are staged in LDS with their row distances
+// (2 bytes per staged token).  Writes the region code (3 evidence, 2 band,
+// 1 context, 0 outside) and the capped distance of the band's tokens, and
+// the largest band distance of the band to band_max (0 when it has none).
 __global__ void __launch_bounds__(kRegionThreads) region_kernel(
-    const uint8_t *__restrict__ evidence, int HW, int W, int ra, int rc,
-    uint8_t *__restrict__ region, uint8_t *__restrict__ dist, int32_t *__restrict__ frame_max) {
+    const uint8_t *__restrict__ evidence, int H, int W, int BR, int nbands, int ra, int rc,
+    uint8_t *__restrict__ region, uint8_t *__restrict__ dist, int32_t *__restrict__ band_max) {
   extern __shared__ uint8_t fr[];
-  uint8_t *ev = fr, *rowd = fr + HW;
   __shared__ int wmax[kRegionThreads / 64];
-  const int64_t base = (int64_t)blockIdx.x * HW;
+  const int frame = blockIdx.x, band = blockIdx.y;
   const int R = ra + rc, cap = R + 1;
+  const int y0 = band * BR, y1 = min(H, y0 + BR);
+  const int ya = max(0, y0 - R), yb = min(H, y1 + R);
+  const int staged = (yb - ya) * W;
+  uint8_t *ev = fr, *rowd = fr + staged;
+  const int64_t base = (int64_t)frame * H * W;
   const int t = threadIdx.x;
-  for (int p = t; p < HW; p += kRegionThreads) ev[p] = evidence[base + p] != 0;
+  for (int p = t; p < staged; p += kRegionThreads) ev[p] = evidence[base + (int64_t)ya * W + p] != 0;
   __syncthreads();
-  for (int p = t; p < HW; p += kRegionThreads) {
-    const int y = p / W, x = p - y * W;
-    const uint8_t *row = ev + y * W;
+  for (int p = t; p < staged; p += kRegionThreads) {
+    const int ly = p / W, x = p - ly * W;
+    const uint8_t *row = ev + ly * W;
     int d = cap;
     for (int k = 0; k <= R; ++k) {
       if ((x - k >= 0 && row[x - k]) || (x + k < W && row[x + k])) {
@@ -54,48 +62,65 @@ __global__ void __launch_bounds__(kRegionThreads) region_kernel(
     rowd[p] = (uint8_t)d;
   }
   __syncthreads();
-  const int H = HW / W;
-  int bandmax = 0;
-  for (int p = t; p < HW; p += kRegionThreads) {
-    const int y = p / W, x = p - y * W;
-    int d = rowd[p];
+  // rows y - k >= 0 and y + k < H within reach lie in [ya, yb)
+  int bmax = 0;
+  for (int p = t; p < (y1 - y0) * W; p += kRegionThreads) {
+    const int y = y0 + p / W, x = p - (p / W) * W;
+    const int q = (y - ya) * W + x;
+    int d = rowd[q];
     for (int k = 1; k <= R && k < d; ++k) {
-      if (y - k >= 0) d = min(d, max(k, (int)rowd[p - k * W]));
-      if (y + k < H) d = min(d, max(k, (int)rowd[p + k * W]));
+      if (y - k >= 0) d = min(d, max(k, (int)rowd[q - k * W]));
+      if (y + k < H) d = min(d, max(k, (int)rowd[q + k * W]));
     }
     const uint8_t code = d == 0 ? 3 : d <= ra ? 2 : d <= R ? 1 : 0;
-    region[base + p] = code;
-    dist[base + p] = (uint8_t)d;
-    if (code == 2) bandmax = max(bandmax, d);
+    region[base + (int64_t)y * W + x] = code;
+    dist[base + (int64_t)y * W + x] = (uint8_t)d;
+    if (code == 2) bmax = max(bmax, d);
   }
   // workgroup maximum
-  for (int o = 32; o > 0; o >>= 1) bandmax = max(bandmax, __shfl_xor(bandmax, o));
-  if ((t & 63) == 0) wmax[t >> 6] = bandmax;
+  for (int o = 32; o > 0; o >>= 1) bmax = max(bmax, __shfl_xor(bmax, o));
+  if ((t & 63) == 0) wmax[t >> 6] = bmax;
   __syncthreads();
   if (t == 0) {
     int m = 0;
     for (int w = 0; w < kRegionThreads / 64; ++w) m = max(m, wmax[w]);
-    frame_max[blockIdx.x] = m;
+    band_max[(int64_t)frame * nbands + band] = m;
   }
 }
 
 // One thread per token: W from the region code, the distance and the band
-// maximum over the frames of the token's batch entry.
+// maximum over the bands (of every frame) of the token's batch entry.  The
+// workgroup first takes that maximum for each batch entry its tokens belong
+// to (usually one), all threads sharing the walk over the nper band maxima.
 __global__ void __launch_bounds__(256) weight_kernel(const uint8_t *__restrict__ region,
                                                      const uint8_t *__restrict__ dist,
-                                                     const int32_t *__restrict__ frame_max,
-                                                     int T, int64_t per_batch, int64_t total,
+                                                     const int32_t *__restrict__ band_max,
+                                                     int nper, int64_t per_batch, int64_t total,
                                                      float *__restrict__ weight) {
-  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  __shared__ int wm[4];
+  const int t = threadIdx.x;
+  const int64_t x0 = (int64_t)blockIdx.x * 256;
+  const int64_t x = x0 + t;
+  const int64_t xl = (x0 + 255 < total ? x0 + 255 : total - 1);
+  const int64_t b0 = x0 / per_batch, b1 = xl / per_batch;
+  const int64_t myb = (x < total ? x : xl) / per_batch;
+  int m = 1;
+  for (int64_t bb = b0; bb <= b1; ++bb) {
+    int v = 0;
+    for (int f = t; f < nper; f += 256) v = max(v, band_max[bb * nper + f]);
+    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
+    if ((t & 63) == 0) wm[t >> 6] = v;
+    __syncthreads();
+    v = max(max(wm[0], wm[1]), max(wm[2], wm[3]));
+    __syncthreads();
+    if (bb == myb) m = max(m, v);
+  }
   if (x >= total) return;
-  const int b = (int)(x / per_batch);
   const uint8_t code = region[x];
   float w = 0.f;
   if (code == 3) {
     w = 1.f;
   } else if (code == 2) {
-    int m = 1;
-    for (int f = 0; f < T; ++f) m = max(m, frame_max[b * T + f]);
     const float s = (float)dist[x] / (float)m;
     w = 1.f - s * s * (3.f - 2.f * s);
   }
@@ -191,24 +216,38 @@ __global__ void __launch_bounds__(256) block_flags_kernel(const uint8_t *__restr
 size_t region_frame_lds(int H, int W) { return (size_t)2 * H * W; }
 
 size_t region_scratch_bytes(int B, int T, int H, int W) {
-  return align_up((size_t)B * T * H * W) + align_up((size_t)B * T * sizeof(int32_t));
+  return align_up((size_t)B * T * H * W) + align_up((size_t)B * T * H * sizeof(int32_t));
+}
+
+// Bands per frame: enough workgroups for every CU to take about two
+// (B T nbands >= 512 when the frames have the rows), at most one band per row.
+static int region_bands(int BT, int H) {
+  int nb = (512 + BT - 1) / BT;
+  nb = nb < 1 ? 1 : (nb > H ? H : nb);
+  const int BR = (H + nb - 1) / nb;
+  return (H + BR - 1) / BR;
 }
 
 hipError_t launch_regions(const uint8_t *evidence, int B, int T, int H, int W, int ra, int rc,
                           uint8_t *region, float *weight, void *scratch, hipStream_t s) {
   const int HW = H * W;
   uint8_t *dist = static_cast<uint8_t *>(scratch);
-  int32_t *fmax = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) +
+  int32_t *bmax = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) +
                                               align_up((size_t)B * T * HW));
-  const size_t lds = region_frame_lds(H, W);
+  const int nbands = region_bands(B * T, H);
+  const int BR = (H + nbands - 1) / nbands;
+  // staged rows: the band and R rows on either side, within the frame
+  const int R = ra + rc;
+  const int staged_rows = BR + 2 * R < H ? BR + 2 * R : H;
+  const size_t lds = (size_t)2 * staged_rows * W;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&region_kernel),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(region_kernel, dim3((unsigned)(B * T)), dim3(kRegionThreads), lds, s,
-                     evidence, HW, W, ra, rc, region, dist, fmax);
+  hipLaunchKernelGGL(region_kernel, dim3((unsigned)(B * T), (unsigned)nbands), dim3(kRegionThreads),
+                     lds, s, evidence, H, W, BR, nbands, ra, rc, region, dist, bmax);
   const int64_t per = (int64_t)T * HW, total = (int64_t)B * per;
   hipLaunchKernelGGL(weight_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, region,
-                     dist, fmax, T, per, total, weight);
+                     dist, bmax, T * nbands, per, total, weight);
   return hipGetLastError();
 }
 
