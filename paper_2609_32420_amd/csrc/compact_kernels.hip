@@ -15,8 +15,13 @@
 // words, so a stored mask is never modified.
 #include "internal.h"
 
+#include <type_traits>
+
 namespace carnator {
 namespace {
+
+// Rows per chunk of the row sort (one thread per row of a chunk).
+constexpr int kChunk = 1024;
 
 // One thread per mask byte.
 __global__ void __launch_bounds__(256) merge_kernel(uint8_t *__restrict__ mask, int H, int nB,
@@ -45,41 +50,6 @@ __device__ inline void load_row(const uint8_t *row, int nB, int lane, uint8_t (&
   for (int c = 0; c < NC; ++c) v[c] = row[min(c * 64 + lane, nB - 1)];
 #pragma unroll
   for (int c = 0; c < NC; ++c) v[c] = c * 64 + lane < nB ? v[c] : 0;
-}
-
-// One wave per row: number of kept key blocks.
-template <int NC>
-__global__ void __launch_bounds__(256) count_kernel(const uint8_t *__restrict__ mask, int64_t R,
-                                                    int nB, int32_t *__restrict__ len) {
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (r >= R) return;
-  uint8_t v[NC];
-  load_row(mask + r * nB, nB, lane, v);
-  int n = 0;
-#pragma unroll
-  for (int c = 0; c < NC; ++c) n += __popcll(__ballot(v[c] != 0));
-  if (lane == 0) len[r] = n;
-}
-
-// One wave per row: ascending kept key blocks at col_idx[row_ptr[r] ...].
-template <int NC>
-__global__ void __launch_bounds__(256) fill_kernel(const uint8_t *__restrict__ mask, int64_t R,
-                                                   int nB, const int32_t *__restrict__ row_ptr,
-                                                   int32_t *__restrict__ col_idx) {
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (r >= R) return;
-  uint8_t v[NC];
-  load_row(mask + r * nB, nB, lane, v);
-  int pos = row_ptr[r];
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const bool kept = v[c] != 0;
-    const unsigned long long bits = __ballot(kept);
-    if (kept) col_idx[pos + __popcll(bits & ((1ull << lane) - 1ull))] = c * 64 + lane;
-    pos += __popcll(bits);
-  }
 }
 
 // ---- bit-packed masks
@@ -187,29 +157,31 @@ __global__ void __launch_bounds__(256) count_bits_kernel(const uint64_t *__restr
 // One wave per row: ascending kept key blocks at col_idx[row_ptr[r] ...].
 // Lane c < nw holds word c; chunk c is broadcast and each lane writes its
 // column when its bit is set, at the count of set bits below it.
-__global__ void __launch_bounds__(256) fill_bits_kernel(const uint64_t *__restrict__ bits, int R,
-                                                        int nB, int HnB,
-                                                        const uint8_t *__restrict__ rows,
-                                                        const uint64_t *__restrict__ colw,
-                                                        bool narrow,
-                                                        const int32_t *__restrict__ row_ptr,
-                                                        int32_t *__restrict__ col_idx) {
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (r >= R || !row_kept((int)r, nB, HnB, rows, narrow)) return;
-  const int nw = (nB + 63) / 64;
-  const uint64_t mine =
-      lane < nw ? merged_word(bits, (int)r, lane, nB, nw, HnB, rows, colw, narrow) : 0ull;
-  const uint64_t below = (1ull << lane) - 1ull;
-  int pos = row_ptr[r];
-  for (int c = 0; c < nw; ++c) {
-    const uint64_t w = read_lane(mine, c);
-    if ((w >> lane) & 1ull) col_idx[pos + __popcll(w & below)] = c * 64 + lane;
-    pos += __popcll(w);
+struct FillBits {
+  const uint64_t *bits;
+  int R, nB, HnB;
+  const uint8_t *rows;
+  const uint64_t *colw;
+  bool narrow;
+  const int32_t *coff, *rloc;
+  int32_t *col_idx;
+  __device__ void operator()(int64_t r, int lane, int *) const {
+    if (r >= R || !row_kept((int)r, nB, HnB, rows, narrow)) return;
+    const int nw = (nB + 63) / 64;
+    const uint64_t mine =
+        lane < nw ? merged_word(bits, (int)r, lane, nB, nw, HnB, rows, colw, narrow) : 0ull;
+    const uint64_t below = (1ull << lane) - 1ull;
+    int pos = coff[r / kChunk] + rloc[r];
+    for (int c = 0; c < nw; ++c) {
+      const uint64_t w = read_lane(mine, c);
+      if ((w >> lane) & 1ull) col_idx[pos + __popcll(w & below)] = c * 64 + lane;
+      pos += __popcll(w);
+    }
   }
-}
+};
 
 constexpr int kScanThreads = 1024;
+static_assert(kChunk == kScanThreads, "one sort thread per row of a chunk");
 
 // Inclusive scan over the 64 lanes of a wave: four DPP row shifts (by 1, 2,
 // 4, 8 lanes; lanes shifted in from outside the 16-lane row read 0) scan each
@@ -244,206 +216,191 @@ __device__ int block_excl_scan(int v, int *sh, int *total) {
   return before;
 }
 
-// LDS budget of the counting sort: its counters and, when they fit beside
-// them, the row lengths.
-constexpr size_t kCountSortLds = 152 * 1024;
-
-// Single workgroup: row_ptr = exclusive scan of the list lengths, and the
-// order of rows by descending length (lower row first on equal lengths) as a
-// counting sort on the length.  Wave w owns the contiguous rows
-// [w C, (w + 1) C) and walks them 64 at a time in row order.
-//   row_ptr: each wave sums its rows, the 16 wave totals give each wave its
-//     first offset, and a second walk writes the offsets with wave scans.
-//   order: pass 1 counts rows per (length, wave) with LDS atomics; an
-//     exclusive scan in (length descending, wave) order turns the counts into
-//     the first slot of each (length, wave) group; pass 2 walks the rows again
-//     in order: lanes holding equal lengths find each other with one ballot
-//     per key bit, each takes its group's next slot plus its rank among those
-//     lanes, and the lowest of them advances the counter.  Lengths descend,
-//     waves and rows ascend: the order the oracle defines.
-// A length of -1 marks a row left out of a restricted call: its list is
-// empty and it sorts after every row of length >= 0 (key nB + 1), in row
-// order; *n_active (when not NULL) receives the number of the other rows,
-// which the exclusive scan leaves as the first slot of key nB + 1.
-// LDS: uint32 counters [nB + 2][16] (index (nB - L) 16 + w), then with
-// LEN_LDS the lengths as int16 [R]; otherwise they are read from len_g.
-template <bool LEN_LDS>
-__global__ void __launch_bounds__(kScanThreads) count_sort_kernel(const int32_t *__restrict__ len_g,
-                                                                  int R, int nB,
-                                                                  int32_t *__restrict__ row_ptr,
-                                                                  int32_t *__restrict__ order,
-                                                                  int32_t *__restrict__ n_active) {
-  constexpr int kWaves = kScanThreads / 64;
-  __shared__ int sh[kWaves];
-  extern __shared__ uint32_t cnt[];
-  const int K = (nB + 2) * kWaves;
-  int16_t *len16 = reinterpret_cast<int16_t *>(cnt + K);
-  const int t = threadIdx.x, lane = t & 63;
-  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
-  for (int i = t; i < K; i += kScanThreads) cnt[i] = 0;
-  if constexpr (LEN_LDS) {
-    // eight loads in flight per thread, clamped indices
-    for (int r0 = 0; r0 < R; r0 += 8 * kScanThreads) {
-      int v[8];
+// ---- compaction of uint8 masks
+//
+// A row of nB mask bytes as aligned 16-byte chunks: lane l loads chunk
+// l + 64 u (u < NU) of the span, so a row costs one 16-byte load per lane
+// and round.  keep[u] holds one bit per byte of the chunk, set for a nonzero
+// byte inside the row; col0[u] is the column of the chunk's first byte
+// (negative when the row starts inside it).  Bytes outside the row are
+// read (they lie in the same aligned 16 bytes as row bytes) but not used.
+template <int NU>
+__device__ inline void load_row16(const uint8_t *row, int nB, int lane, uint32_t (&keep)[NU],
+                                  int (&col0)[NU]) {
+  const uintptr_t p = reinterpret_cast<uintptr_t>(row);
+  const uintptr_t pa = p & ~(uintptr_t)15;
+  const int head = (int)(p - pa);  // row bytes start at this byte of chunk 0
+  const int nch = (head + nB + 15) >> 4;
+  uint4 w[NU];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int r = r0 + u * kScanThreads + t;
-        v[u] = len_g[r < R ? r : R - 1];
-      }
+  for (int u = 0; u < NU; ++u) {
+    const int c = min(u * 64 + lane, nch - 1);
+    w[u] = *reinterpret_cast<const uint4 *>(pa + 16 * (uintptr_t)c);
+  }
+  // bit 7 of each byte: set when the byte is nonzero; then the four bytes'
+  // flags of a word gathered into 4 bits
+  auto nz4 = [](uint32_t x) __attribute__((always_inline)) {
+    const uint32_t f = (((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x) & 0x80808080u;
+    return ((f >> 7) & 1u) | ((f >> 14) & 2u) | ((f >> 21) & 4u) | ((f >> 28) & 8u);
+  };
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int r = r0 + u * kScanThreads + t;
-        if (r < R) len16[r] = (int16_t)v[u];
-      }
-    }
-  }
-  __syncthreads();
-  auto lenv = [&](int r) __attribute__((always_inline)) -> int {
-    if constexpr (LEN_LDS) return len16[r];
-    else return len_g[r];
-  };
-  const int C = (R + kWaves - 1) / kWaves;
-  const int rlo = min(R, w * C), rhi = min(R, rlo + C);
-
-  // ---- row_ptr
-  {
-    int part = 0;
-    for (int r0 = rlo; r0 < rhi; r0 += 64) {
-      const int r = r0 + lane;
-      part += r < rhi ? max(lenv(r), 0) : 0;
-    }
-    const int wtot = __builtin_amdgcn_readlane(wave_incl_scan(part), 63);
-    if (lane == 0) sh[w] = wtot;
-    __syncthreads();
-    int off = 0, total = 0;
-    for (int q = 0; q < kWaves; ++q) {
-      const int c = sh[q];
-      off += q < w ? c : 0;
-      total += c;
-    }
-    for (int r0 = rlo; r0 < rhi; r0 += 64) {
-      const int r = r0 + lane;
-      const int v = r < rhi ? max(lenv(r), 0) : 0;
-      const int incl = wave_incl_scan(v);
-      if (r < rhi) row_ptr[r] = off + incl - v;
-      off += __builtin_amdgcn_readlane(incl, 63);
-    }
-    if (t == 0) row_ptr[R] = total;
-  }
-
-  // ---- order
-  int kbits = 0;
-  while ((1 << kbits) <= nB + 1) ++kbits;
-  // the lanes of this walk step holding the same key (nB - length) as this lane
-  auto peers_of = [&](bool on, int key) __attribute__((always_inline)) {
-    unsigned long long m = __ballot(on);
-    for (int b = 0; b < kbits; ++b) {
-      const unsigned long long ones = __ballot(on && ((key >> b) & 1));
-      m &= ((key >> b) & 1) ? ones : ~ones;
-    }
-    return m;
-  };
-  for (int r0 = rlo; r0 < rhi; r0 += 64) {
-    const int r = r0 + lane;
-    if (r < rhi) atomicAdd(&cnt[(nB - lenv(r)) * kWaves + w], 1u);
-  }
-  __syncthreads();
-  {
-    // exclusive scan of the counters in index order, a contiguous segment per
-    // thread
-    const int per = (K + kScanThreads - 1) / kScanThreads;
-    const int lo = min(K, per * t), hi = min(K, lo + per);
-    int local = 0;
-    for (int i = lo; i < hi; ++i) local += (int)cnt[i];
-    int total;
-    int run = block_excl_scan(local, sh, &total);
-    for (int i = lo; i < hi; ++i) {
-      const int c = (int)cnt[i];
-      cnt[i] = (uint32_t)run;
-      run += c;
-    }
-  }
-  __syncthreads();
-  // (wave 0 reads the slot before its own pass-2 updates; other waves never
-  // update counter (nB + 1) 16 + 0)
-  if (t == 0 && n_active != nullptr) *n_active = (int32_t)cnt[(nB + 1) * kWaves];
-  for (int r0 = rlo; r0 < rhi; r0 += 64) {
-    const int r = r0 + lane;
-    const bool on = r < rhi;
-    const int key = on ? nB - lenv(r) : 0;
-    const unsigned long long m = peers_of(on, key);
-    if (on) {
-      uint32_t &c = cnt[key * kWaves + w];
-      order[(int)c + __popcll(m & ((1ull << lane) - 1ull))] = r;
-      // every lane of the group has read the counter before the lowest lane
-      // writes it back (one wave: its LDS accesses complete in program order)
-      if (lane == __builtin_ctzll(m)) c += (uint32_t)__popcll(m);
-    }
+  for (int u = 0; u < NU; ++u) {
+    const int c = u * 64 + lane;
+    const int off = 16 * c - head;
+    const int lo = max(0, -off), hi = min(16, nB - off);
+    const uint32_t valid = (c < nch && hi > lo) ? (((1u << hi) - 1u) & ~((1u << lo) - 1u)) : 0u;
+    const uint32_t f = nz4(w[u].x) | (nz4(w[u].y) << 4) | (nz4(w[u].z) << 8) | (nz4(w[u].w) << 12);
+    keep[u] = f & valid;
+    col0[u] = off;
   }
 }
 
-// ---- the same row_ptr and order by several workgroups (chunks of kChunk rows)
+// One wave per row: number of kept key blocks.
+template <int NU>
+__global__ void __launch_bounds__(256) count_kernel(const uint8_t *__restrict__ mask, int64_t R,
+                                                    int nB, int32_t *__restrict__ len) {
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= R) return;
+  uint32_t keep[NU];
+  int col0[NU];
+  load_row16<NU>(mask + r * nB, nB, lane, keep, col0);
+  int n = 0;
+#pragma unroll
+  for (int u = 0; u < NU; ++u) n += __popc(keep[u]);
+  n = __builtin_amdgcn_readlane(wave_incl_scan(n), 63);
+  if (lane == 0) len[r] = n;
+}
+
+// One wave per row (row r, lane lane): ascending kept key blocks from
+// col_idx[row_ptr[r]] on, row_ptr[r] being the offset of r's chunk of rows
+// plus its prefix inside the chunk (both written by the sort).  A lane
+// writes its 16 bytes' columns into the wave's LDS staging area (nB + 2
+// ints) at the count of kept columns in the lanes below it (a wave scan);
+// the wave then copies the list out, 64 consecutive entries per store.
+template <int NU>
+struct FillBytes {
+  const uint8_t *mask;
+  int64_t R;
+  int nB;
+  const int32_t *coff, *rloc;
+  int32_t *col_idx;
+  __device__ void operator()(int64_t r, int lane, int *stage) const {
+    if (r >= R) return;
+    uint32_t keep[NU];
+    int col0[NU];
+    load_row16<NU>(mask + r * nB, nB, lane, keep, col0);
+    const int pos = coff[r / kChunk] + rloc[r];
+    int n = 0;
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int cnt = __popc(keep[u]);
+      const int incl = wave_incl_scan(cnt);
+      int q = n + incl - cnt;
+      for (uint32_t k = keep[u]; k != 0u; k &= k - 1u) stage[q++] = col0[u] + __builtin_ctz(k);
+      n += __builtin_amdgcn_readlane(incl, 63);
+    }
+    // one wave: its LDS writes complete before its reads
+    for (int i = lane; i < n; i += 64) col_idx[pos + i] = stage[i];
+  }
+};
+
+// ---- row_ptr and the order of rows by descending list length
 //
+// Sort key of a row: nB - length, so that longer lists come first, and
+// nB + 1 for a row a restriction leaves out (length -1: an empty list,
+// placed after every other row).  Rows come in G chunks of kChunk rows.
 //   sort_hist_kernel, one workgroup per chunk g: the chunk's key histogram
-//     (key = nB - length, nB + 1 for a left-out row) to hist[g K + key],
-//     K = nB + 2, and its length sum to csum[g];
+//     to hist[g K + key] (K = nB + 2), each row's exclusive prefix of the
+//     lengths inside the chunk to rloc, the chunk's length sum to csum[g];
 //   sort_scan_kernel, one workgroup: for each key, the exclusive prefix of
 //     its counts over the chunks plus the exclusive prefix of the key totals
-//     (key order) -- the first slot of chunk g's rows of each key -- and the
-//     exclusive scan of csum;
-//   sort_place_kernel, one workgroup per chunk: row_ptr of its rows (chunk
-//     offset plus a block scan), and each row's slot in order: its chunk's
-//     first slot for its key, plus the rows of that key in earlier waves of
-//     the chunk (per-wave counts, scanned per key), plus the lanes below it
-//     in its wave holding the same key (one ballot per key bit).
+//     (key order) -- the first slot in order of chunk g's rows of each key,
+//     in place of hist -- the exclusive scan of csum in place (the chunk
+//     offsets of row_ptr), row_ptr[R] and *n_active (the first slot of key
+//     nB + 1: the number of rows not left out);
+//   place_fill_kernel, workgroups 0 .. G - 1, one per chunk: row_ptr of its
+//     rows (chunk offset plus rloc), and each row's slot in order: its
+//     chunk's first slot for its key, plus the rows of that key in earlier
+//     waves of the chunk (per-wave counts, scanned per key), plus the lanes
+//     below it in its wave holding the same key (one ballot per key bit).
+//     The other workgroups write col_idx, one wave per row, from the same
+//     chunk offset and rloc: the two parts share the launch and nothing
+//     else.
 // Within a chunk wave w holds rows 64 w .. 64 w + 63 in row order, so rows
 // of equal key keep their row order: the order the oracle defines.
-constexpr int kChunk = 1024;
+constexpr int kSortWaves = kScanThreads / 64;
 
 __device__ inline int sort_key(int L, int nB) { return L < 0 ? nB + 1 : nB - L; }
 
 __global__ void __launch_bounds__(kScanThreads) sort_hist_kernel(const int32_t *__restrict__ len,
-                                                                 int R, int nB, int G,
+                                                                 int R, int nB,
                                                                  int32_t *__restrict__ hist,
-                                                                 int32_t *__restrict__ csum) {
+                                                                 int32_t *__restrict__ csum,
+                                                                 int32_t *__restrict__ rloc) {
   extern __shared__ int hk[];  // nB + 2 counters
-  __shared__ int sh[kScanThreads / 64];
+  __shared__ int sh[kSortWaves];
   const int g = blockIdx.x, t = threadIdx.x;
-  for (int k = t; k < nB + 2; k += kScanThreads) hk[k] = 0;
+  const int K = nB + 2;
+  for (int k = t; k < K; k += kScanThreads) hk[k] = 0;
   __syncthreads();
   const int r = g * kChunk + t;
   const int L = r < R ? len[r] : 0;
   if (r < R) atomicAdd(&hk[sort_key(L, nB)], 1);
   int total;
-  (void)block_excl_scan(max(L, 0), sh, &total);
-  for (int k = t; k < nB + 2; k += kScanThreads) hist[(int64_t)g * (nB + 2) + k] = hk[k];
+  const int ex = block_excl_scan(max(L, 0), sh, &total);  // ends with a barrier
+  if (r < R) rloc[r] = ex;
+  for (int k = t; k < K; k += kScanThreads) hist[(int64_t)g * K + k] = hk[k];
   if (t == 0) csum[g] = total;
 }
 
 // One workgroup, thread t owning keys t, t + 1024, t + 2048: the chunk
-// prefix of each of its keys (G coalesced loads and stores per key, eight
-// loads in flight), then the key totals scanned in key order one pass of
-// 1024 keys at a time and added back; the chunk offsets of row_ptr, row_ptr[R]
-// and the number of rows not left out (the first slot of key nB + 1).
+// counts of each of its keys (coalesced over the threads), the key totals
+// scanned in key order one pass of 1024 keys at a time, and each count
+// replaced by the key's first slot in that chunk.  Up to 32 chunks
+// the counts stay in registers (one round trip; REGS >= G, the smallest of
+// 4, 8, 16, 32); beyond, they are rewritten as prefixes sixteen loads at a
+// time and the key offset added in a second pass.  Then the chunk offsets.
+template <int REGS>
 __global__ void __launch_bounds__(kScanThreads) sort_scan_kernel(int R, int nB, int G,
                                                                  int32_t *__restrict__ hist,
                                                                  int32_t *__restrict__ csum,
                                                                  int32_t *__restrict__ row_ptr,
                                                                  int32_t *__restrict__ n_active) {
-  __shared__ int sh[kScanThreads / 64];
+  __shared__ int sh[kSortWaves];
   const int t = threadIdx.x;
   const int K = nB + 2;
   int carry = 0;
   for (int k0 = 0; k0 < K; k0 += kScanThreads) {
     const int k = k0 + t;
+    if (G <= REGS) {
+      // every chunk count of the key in registers, all loads in flight
+      int v[REGS];
+#pragma unroll
+      for (int u = 0; u < REGS; ++u) v[u] = (k < K && u < G) ? hist[(int64_t)u * K + k] : 0;
+      int tot = 0;
+#pragma unroll
+      for (int u = 0; u < REGS; ++u) tot += v[u];
+      int all;
+      int run = block_excl_scan(tot, sh, &all) + carry;
+      carry += all;
+      if (k < K) {
+#pragma unroll
+        for (int u = 0; u < REGS; ++u) {
+          if (u < G) hist[(int64_t)u * K + k] = run;
+          run += v[u];
+        }
+      }
+      continue;
+    }
     int tot = 0;
     if (k < K) {
-      for (int g0 = 0; g0 < G; g0 += 8) {
-        int v[8];
+      for (int g0 = 0; g0 < G; g0 += 16) {
+        int v[16];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = g0 + u < G ? hist[(int64_t)(g0 + u) * K + k] : 0;
+        for (int u = 0; u < 16; ++u) v[u] = g0 + u < G ? hist[(int64_t)(g0 + u) * K + k] : 0;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < 16; ++u) {
           if (g0 + u < G) hist[(int64_t)(g0 + u) * K + k] = tot;
           tot += v[u];
         }
@@ -474,34 +431,41 @@ __global__ void __launch_bounds__(kScanThreads) sort_scan_kernel(int R, int nB, 
   }
 }
 
-__global__ void __launch_bounds__(kScanThreads) sort_place_kernel(const int32_t *__restrict__ len,
+template <class Fill>
+__global__ void __launch_bounds__(kScanThreads) place_fill_kernel(const int32_t *__restrict__ len,
                                                                   int R, int nB, int G,
                                                                   const int32_t *__restrict__ base,
                                                                   const int32_t *__restrict__ coff,
+                                                                  const int32_t *__restrict__ rloc,
                                                                   int32_t *__restrict__ row_ptr,
-                                                                  int32_t *__restrict__ order) {
-  constexpr int kWaves = kScanThreads / 64;
-  extern __shared__ int wc[];  // (nB + 2) * kWaves per-wave counts, then slots
-  __shared__ int sh[kWaves];
-  const int g = blockIdx.x, t = threadIdx.x, lane = t & 63;
+                                                                  int32_t *__restrict__ order,
+                                                                  Fill fill) {
+  extern __shared__ int wc[];  // (nB + 2) * kSortWaves per-wave counts, then slots
+  const int t = threadIdx.x, lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   const int K = nB + 2;
-  for (int i = t; i < K * kWaves; i += kScanThreads) wc[i] = 0;
+  if ((int)blockIdx.x >= G) {
+    // a filling workgroup: nB + 2 ints of staging per wave
+    fill(((int64_t)blockIdx.x - G) * kSortWaves + w, lane, wc + w * K);
+    return;
+  }
+  const int g = blockIdx.x;
+  for (int i = t; i < K * kSortWaves; i += kScanThreads) wc[i] = 0;
   __syncthreads();
   const int r = g * kChunk + t;
   const bool on = r < R;
-  const int L = on ? len[r] : 0;
-  const int key = on ? sort_key(L, nB) : 0;
-  if (on) atomicAdd(&wc[key * kWaves + w], 1);
-  int total;
-  const int ex = block_excl_scan(on ? max(L, 0) : 0, sh, &total);  // ends with a barrier
-  if (on) row_ptr[r] = coff[g] + ex;
+  const int key = on ? sort_key(len[r], nB) : 0;
+  if (on) {
+    atomicAdd(&wc[key * kSortWaves + w], 1);
+    row_ptr[r] = coff[g] + rloc[r];
+  }
+  __syncthreads();
   for (int k = t; k < K; k += kScanThreads) {
     int run = base[(int64_t)g * K + k];
 #pragma unroll
-    for (int q = 0; q < kWaves; ++q) {
-      const int c = wc[k * kWaves + q];
-      wc[k * kWaves + q] = run;
+    for (int q = 0; q < kSortWaves; ++q) {
+      const int c = wc[k * kSortWaves + q];
+      wc[k * kSortWaves + q] = run;
       run += c;
     }
   }
@@ -513,7 +477,7 @@ __global__ void __launch_bounds__(kScanThreads) sort_place_kernel(const int32_t 
     const unsigned long long ones = __ballot(on && ((key >> b) & 1));
     m &= ((key >> b) & 1) ? ones : ~ones;
   }
-  if (on) order[wc[key * kWaves + w] + __popcll(m & ((1ull << lane) - 1ull))] = r;
+  if (on) order[wc[key * kSortWaves + w] + __popcll(m & ((1ull << lane) - 1ull))] = r;
 }
 
 }  // namespace
@@ -528,63 +492,71 @@ hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows
 
 static int sort_chunks(int64_t R) { return (int)((R + kChunk - 1) / kChunk); }
 
-// Lengths, then the chunk histograms and offsets of the multi-workgroup sort.
+// The list lengths, then the chunk histograms (key offsets after the scan),
+// the chunk length sums (chunk offsets after the scan) and the in-chunk
+// prefixes of the lengths.
 size_t compact_scratch_bytes(int64_t R, int nB) {
-  const int G = sort_chunks(R);
-  return align_up((size_t)R * sizeof(int32_t)) + align_up((size_t)(nB + 2) * G * sizeof(int32_t)) +
+  if (R <= 0) return 0;
+  const int64_t G = sort_chunks(R);
+  return 2 * align_up((size_t)R * sizeof(int32_t)) + align_up((size_t)(nB + 2) * G * sizeof(int32_t)) +
          align_up((size_t)G * sizeof(int32_t));
 }
 
-// Rows up to which the single-workgroup counting sort runs (one launch);
-// beyond, the chunked sort (three launches) spreads the walk over the CUs.
-constexpr int64_t kSingleSortRows = 4096;
-
-// row_ptr and order from the list lengths; sort_scratch: the histogram and
-// chunk offsets of compact_scratch_bytes.
-static hipError_t launch_sort(const int32_t *len, int64_t R, int nB, int32_t *row_ptr, int32_t *order,
-                              int32_t *n_active, void *sort_scratch, hipStream_t s) {
-  if (R > kSingleSortRows) {
-    const int G = sort_chunks(R);
-    int32_t *hist = static_cast<int32_t *>(sort_scratch);
-    int32_t *csum = reinterpret_cast<int32_t *>(static_cast<char *>(sort_scratch) +
-                                                align_up((size_t)(nB + 2) * G * sizeof(int32_t)));
-    const size_t hl = (size_t)(nB + 2) * sizeof(int32_t);
-    const size_t pl = (size_t)(nB + 2) * (kScanThreads / 64) * sizeof(int32_t);
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sort_place_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(sort_hist_kernel, dim3((unsigned)G), dim3(kScanThreads), hl, s, len, (int)R, nB,
-                       G, hist, csum);
-    hipLaunchKernelGGL(sort_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, (int)R, nB, G, hist, csum,
-                       row_ptr, n_active);
-    hipLaunchKernelGGL(sort_place_kernel, dim3((unsigned)G), dim3(kScanThreads), pl, s, len, (int)R, nB,
-                       G, hist, csum, row_ptr, order);
-    return hipGetLastError();
-  }
-  const size_t cnt_lds = (size_t)(nB + 2) * (kScanThreads / 64) * sizeof(uint32_t);
-  const size_t len_lds = (size_t)R * sizeof(int16_t);
-  hipError_t e;
-  if (cnt_lds + len_lds <= kCountSortLds) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void *>(&count_sort_kernel<true>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)(cnt_lds + len_lds));
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(count_sort_kernel<true>, dim3(1), dim3(kScanThreads), cnt_lds + len_lds, s,
-                       len, (int)R, nB, row_ptr, order, n_active);
-  } else {
-    e = hipFuncSetAttribute(reinterpret_cast<const void *>(&count_sort_kernel<false>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)cnt_lds);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(count_sort_kernel<false>, dim3(1), dim3(kScanThreads), cnt_lds, s, len,
-                       (int)R, nB, row_ptr, order, n_active);
-  }
+// row_ptr and order from the list lengths, then col_idx by `fill` (built by
+// make_fill from the chunk offsets and in-chunk prefixes); sort_scratch: the
+// part of compact_scratch_bytes after the lengths.
+template <class MakeFill>
+static hipError_t launch_sort_fill(const int32_t *len, int64_t R, int nB, int32_t *row_ptr,
+                                   int32_t *order, int32_t *n_active, void *sort_scratch,
+                                   const MakeFill &make_fill, hipStream_t s) {
+  const int G = sort_chunks(R);
+  const int K = nB + 2;
+  char *p = static_cast<char *>(sort_scratch);
+  int32_t *hist = reinterpret_cast<int32_t *>(p);
+  p += align_up((size_t)K * G * sizeof(int32_t));
+  int32_t *csum = reinterpret_cast<int32_t *>(p);
+  p += align_up((size_t)G * sizeof(int32_t));
+  int32_t *rloc = reinterpret_cast<int32_t *>(p);
+  const auto fill = make_fill(csum, rloc);
+  using Fill = std::decay_t<decltype(fill)>;
+  const size_t hl = (size_t)K * sizeof(int32_t);
+  const size_t pl = (size_t)K * kSortWaves * sizeof(int32_t);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&place_fill_kernel<Fill>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(sort_hist_kernel, dim3((unsigned)G), dim3(kScanThreads), hl, s, len, (int)R, nB,
+                     hist, csum, rloc);
+  auto scan = G <= 4 ? sort_scan_kernel<4> : G <= 8 ? sort_scan_kernel<8> : G <= 16 ? sort_scan_kernel<16> : sort_scan_kernel<32>;
+  hipLaunchKernelGGL(scan, dim3(1), dim3(kScanThreads), 0, s, (int)R, nB, G, hist, csum, row_ptr,
+                     n_active);
+  const int64_t fill_groups = (R + kSortWaves - 1) / kSortWaves;
+  hipLaunchKernelGGL(place_fill_kernel<Fill>, dim3((unsigned)(G + fill_groups)), dim3(kScanThreads),
+                     pl, s, len, (int)R, nB, G, hist, csum, rloc, row_ptr, order, fill);
   return hipGetLastError();
 }
 
 hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_ptr,
                           int32_t *col_idx, int32_t *order, void *scratch, hipStream_t s) {
   int32_t *len = static_cast<int32_t *>(scratch);
+  void *sort_scratch = static_cast<char *>(scratch) + align_up((size_t)R * sizeof(int32_t));
   const unsigned g = (unsigned)((R + 3) / 4);
-  const int nc = (nB + 63) / 64;  // nB <= 2048
+  // 16-byte chunks of a row: at most (15 + nB + 15) / 16 (nB <= 2048)
+  const int nu = ((15 + nB + 15) / 16 + 63) / 64;
+#define CARNATOR_COMPACT(NU)                                                                     \
+  do {                                                                                           \
+    hipLaunchKernelGGL(count_kernel<NU>, dim3(g), dim3(256), 0, s, mask, R, nB, len);            \
+    return launch_sort_fill(len, R, nB, row_ptr, order, nullptr, sort_scratch,                   \
+                            [&](const int32_t *coff, const int32_t *rloc) {                      \
+                              return FillBytes<NU>{mask, R, nB, coff, rloc, col_idx};            \
+                            },                                                                   \
+                            s);                                                                  \
+  } while (0)
+  if (nu <= 1) CARNATOR_COMPACT(1);
+  else if (nu <= 2) CARNATOR_COMPACT(2);
+  else CARNATOR_COMPACT(3);
+#undef CARNATOR_COMPACT
+}
+
 #define CARNATOR_ROWS(KERNEL, ...)                                                         \
   do {                                                                                   \
     if (nc <= 4) hipLaunchKernelGGL(KERNEL<4>, dim3(g), dim3(256), 0, s, __VA_ARGS__);   \
@@ -592,13 +564,6 @@ hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_p
     else if (nc <= 16) hipLaunchKernelGGL(KERNEL<16>, dim3(g), dim3(256), 0, s, __VA_ARGS__); \
     else hipLaunchKernelGGL(KERNEL<32>, dim3(g), dim3(256), 0, s, __VA_ARGS__);          \
   } while (0)
-  CARNATOR_ROWS(count_kernel, mask, R, nB, len);
-  hipError_t e = launch_sort(len, R, nB, row_ptr, order, nullptr,
-                             static_cast<char *>(scratch) + align_up((size_t)R * sizeof(int32_t)), s);
-  if (e != hipSuccess) return e;
-  CARNATOR_ROWS(fill_kernel, mask, R, nB, row_ptr, col_idx);
-  return hipGetLastError();
-}
 
 hipError_t launch_pack(const uint8_t *mask, int64_t R, int nB, uint64_t *bits, hipStream_t s) {
   if (R == 0) return hipSuccess;
@@ -654,13 +619,12 @@ hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const
 #undef CARNATOR_G
     default: return hipErrorInvalidValue;
   }
-  if ((e = launch_sort(len, R, nB, row_ptr, order, n_active,
-                       static_cast<char *>(scratch) + align_up((size_t)R * sizeof(int32_t)), s)) !=
-      hipSuccess)
-    return e;
-  hipLaunchKernelGGL(fill_bits_kernel, dim3((unsigned)((R + 3) / 4)), dim3(256), 0, s, bits,
-                     (int)R, nB, HnB, rows, colw, narrow, row_ptr, col_idx);
-  return hipGetLastError();
+  return launch_sort_fill(len, R, nB, row_ptr, order, n_active,
+                          static_cast<char *>(scratch) + align_up((size_t)R * sizeof(int32_t)),
+                          [&](const int32_t *coff, const int32_t *rloc) {
+                            return FillBits{bits, (int)R, nB, HnB, rows, colw, narrow, coff, rloc, col_idx};
+                          },
+                          s);
 }
 
 }  // namespace carnator

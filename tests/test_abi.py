@@ -215,10 +215,10 @@ def test_bit_packed_workspace_size(L):
     s = _shape(1, 12, 32760, 128, 128)
     R = 12 * 256
     # the list lengths, the sort's chunk histograms ((nB + 2) keys x 3 chunks
-    # of 1024 rows) and chunk offsets, then the packed dense-column words of
-    # each batch entry
+    # of 1024 rows), chunk offsets and in-chunk prefixes of the lengths, then
+    # the packed dense-column words of each batch entry
     hist = -(-(258 * 3 * 4) // 256) * 256
-    assert L.carnator_compact_block_mask_bits_workspace_size(ctypes.byref(s)) == 12288 + hist + 256 + 256
+    assert L.carnator_compact_block_mask_bits_workspace_size(ctypes.byref(s)) == 12288 + hist + 256 + 12288 + 256
     assert L.carnator_compact_block_mask_bits_workspace_size(ctypes.byref(_shape(d=96))) == 0
     assert R * 4 == 12288
 
