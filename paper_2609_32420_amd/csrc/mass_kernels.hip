@@ -47,14 +47,18 @@ struct MassState {
   float m_run, l_run, mb, sl;
 };
 
-// Fold one 32-key tile of scores (raw, keys at or past lim masked) into st.
+// Fold one 32-key tile of scores (raw; with MASK, keys at or past lim
+// masked: only the last key block can be partial) into st.
+template <bool MASK>
 __device__ __attribute__((always_inline)) inline void mass_tile(MassState &st, f32x16 acc, int m,
                                                                 int hh, int lim, float c2) {
   float tm = -INFINITY;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
-    const int key = m * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
-    acc[v] = key < lim ? acc[v] : -INFINITY;
+    if constexpr (MASK) {
+      const int key = m * 32 + 8 * (v >> 2) + 4 * hh + (v & 3);
+      acc[v] = key < lim ? acc[v] : -INFINITY;
+    }
     tm = fmaxf(tm, acc[v]);
   }
   tm = fmaxf(tm, __shfl_xor(tm, 32)) * c2;
@@ -175,7 +179,7 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, int bh0, float c2,
   // one key block: LDS buffer jj & 1 holds block jj, S1 holds block jj + 1
   // and S2 block jj + 2 (both in flight); S1 is stored for the next body and
   // refilled with block jj + 3
-#define CARNATOR_MASS_BODY(JJ, S1)                                                       \
+#define CARNATOR_MASS_BODY(JJ, S1, MASK)                                                 \
   {                                                                                      \
     const int jj = (JJ);                                                                 \
     const bool live = jj < nB;                                                           \
@@ -186,8 +190,8 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, int bh0, float c2,
       const int r = m * 32 + l32;                                                        \
       f32x16 acc0, acc1;                                                                 \
       qk_tile2<D, C::CPR>(base + r * C::RB, r, hh, q0, q1, acc0, acc1);                  \
-      mass_tile(s0, acc0, m, hh, lim, c2);                                               \
-      mass_tile(s1, acc1, m, hh, lim, c2);                                               \
+      mass_tile<MASK>(s0, acc0, m, hh, lim, c2);                                         \
+      mass_tile<MASK>(s1, acc1, m, hh, lim, c2);                                         \
     }                                                                                    \
     const float t0 = s0.sl + __shfl_xor(s0.sl, 32), t1 = s1.sl + __shfl_xor(s1.sl, 32);  \
     if (live) {                                                                          \
@@ -204,10 +208,15 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, int bh0, float c2,
     CARNATOR_MASS_LOAD(S1, jj + 3)                                                       \
   }
 
-  for (int j = 0; j < nB; j += 2) {
-    CARNATOR_MASS_BODY(j, sa)
-    CARNATOR_MASS_BODY(j + 1, sb)
+  // every key block but the last is full: the pairs before the one holding
+  // block nB - 1 take no key mask
+  const int jl = (nB - 1) & ~1;
+  for (int j = 0; j < jl; j += 2) {
+    CARNATOR_MASS_BODY(j, sa, false)
+    CARNATOR_MASS_BODY(j + 1, sb, false)
   }
+  CARNATOR_MASS_BODY(jl, sa, true)
+  CARNATOR_MASS_BODY(jl + 1, sb, true)
 #undef CARNATOR_MASS_BODY
 #undef CARNATOR_MASS_LOAD
 #undef CARNATOR_MASS_STORE
