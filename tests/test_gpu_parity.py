@@ -157,10 +157,14 @@ def test_merge_bit_exact(wid):
 
 # R = heads * nb rows.  Up to 4096 rows one workgroup sorts them (counters in
 # LDS, the row lengths beside them while they fit); beyond, chunks of 1024
-# rows are sorted by several workgroups: (931, 5), (2048, *) and the
-# 119K-token shape (931, 24: 22 chunks, the last partial).
+# R = heads * nb rows in chunks of 1024: one chunk up to (931, 1); 3, 5, 10,
+# 14 and 22 chunks (the last partial) keep a key's chunk counts in registers
+# in the scan; (2048, 17) has 34 chunks and takes the two-pass scan.  Rows of
+# 1100 key blocks span two rounds of 16-byte chunks per lane, rows of 2048
+# three.
 @pytest.mark.parametrize("nb,density,heads", [(3, 0.5, 5), (139, 0.3, 5), (256, 0.2, 5), (931, 0.1, 5),
-                                              (2048, 0.05, 5), (2048, 0.05, 7), (931, 0.1, 24),
+                                              (1100, 0.1, 3), (2048, 0.05, 5), (2048, 0.05, 7),
+                                              (931, 0.1, 24), (2048, 0.02, 17),
                                               # every row full but one: one length group in row order
                                               (64, 1.0, 3)])
 def test_compaction_bit_exact(nb, density, heads):
@@ -213,8 +217,8 @@ def test_mask_builder_bits_full_threshold(nb):
     np.testing.assert_array_equal(_u64(bits), oracle.pack_mask(np.ones((1, 2, nb, nb), dtype=np.uint8)))
 
 
-# widened or not; R = heads * nb rows (2048 x 7 reads the lengths from memory
-# in the sort, as for the uint8 compaction)
+# widened or not; R = B * heads * nb rows (2048 x 7 x 2: 28 chunks of the
+# sort)
 @pytest.mark.parametrize("nb,density,heads,widen", [(3, 0.5, 5, False), (139, 0.3, 5, True), (256, 0.2, 5, True),
                                                     (256, 0.2, 5, False), (931, 0.1, 3, True),
                                                     (2048, 0.05, 7, True), (64, 1.0, 3, False)])
