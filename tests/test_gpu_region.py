@@ -64,6 +64,22 @@ def test_region_weights_degenerate_evidence():
     _check_regions(ev)
 
 
+def test_region_weights_batch_entries_share_a_workgroup():
+    # 6 batch entries of 2 x 3 x 7 tokens (252 tokens, one workgroup of the
+    # weight pass) whose band maxima differ: 1 (evidence all but a border),
+    # 2 (one evidence token), none (no evidence) and three random entries
+    ev = np.zeros((6, 2, 3, 7), np.uint8)
+    ev[0, :, 1:2, 1:6] = 1
+    ev[0, 1] = 0
+    ev[1, 0, 1, 3] = 1
+    rng = np.random.default_rng(7)
+    ev[3:] = (rng.random((3, 2, 3, 7)) < 0.1).astype(np.uint8)
+    ev[3, 0, 0, 0] = 1
+    _check_regions(ev)
+    want_code, _ = oracle.regions(ev, 2, 3)
+    assert len({int(x) for x in (want_code == 2).reshape(6, -1).sum(1)}) > 2
+
+
 @pytest.mark.parametrize("wid,channels,patch", [(1, 16, (1, 2, 2)), (0, 4, (1, 1, 1)), (2, 3, (1, 2, 3)),
                                                 (3, 16, (1, 2, 2))])
 def test_latent_fusion(wid, channels, patch):
