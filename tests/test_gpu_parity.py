@@ -428,6 +428,27 @@ def test_attention_ragged_shapes_and_dims(N, bs, d):
     assert torch.equal(o.view(torch.int16), o_plain.view(torch.int16))
 
 
+@pytest.mark.parametrize("N,bs,d", [(131035, 64, 64), (262100, 128, 128)])
+def test_attention_longest_lists(N, bs, d):
+    # nB = 2048, the largest number of key blocks: rows 0, 5 and the last keep
+    # every key block (the longest list a row can have, the ragged tail
+    # included); the others about 5 % of them
+    g = torch.Generator(device=DEV).manual_seed(N)
+    q, k, v = (torch.randn(1, 1, N, d, generator=g, device=DEV).to(torch.bfloat16) for _ in range(3))
+    nb = -(-N // bs)
+    assert nb == 2048
+    m = synth.random_mask(1, 1, nb, 0.05, 5)
+    m[0, 0, [0, 5, nb - 1]] = 1
+    o, lse = P.block_sparse_attn(q, k, v, torch.as_tensor(m, device=DEV), bs, return_lse=True)
+    o_plain = P.block_sparse_attn(q, k, v, torch.as_tensor(m, device=DEV), bs)
+    torch.cuda.synchronize()
+    rows = [(0, 0, i) for i in (0, 5, 700, 1500, nb - 1)]
+    ro, rl = oracle.block_sparse_attention(oracle.to_f64(q), oracle.to_f64(k), oracle.to_f64(v), m, bs,
+                                           rows=rows)
+    _compare_rows(o, ro, lse, rl, rows, N, bs)
+    _compare_rows(o_plain, ro, None, None, rows, N, bs)
+
+
 def test_attention_empty_rows_and_explicit_scale():
     N, bs, d = 512, 128, 128
     g = torch.Generator(device=DEV).manual_seed(11)
