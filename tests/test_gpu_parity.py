@@ -123,8 +123,10 @@ def test_mask_builder_thresholds_and_explicit_scale(tau):
 
 
 @pytest.mark.parametrize("N,bs,d", [(50, 64, 64), (1000, 64, 128), (4100, 128, 64), (9000, 64, 64),
-                                   (22350, 64, 64), (47300, 64, 128), (70000, 64, 64), (102380, 64, 64)])
+                                   (22350, 64, 64), (47300, 64, 128), (70000, 64, 64), (102380, 64, 64),
+                                   (131032, 64, 64)])
 def test_mask_builder_ragged_random(N, bs, d):
+    # up to nB = 2048 key blocks (131032 tokens of block 64), the largest
     g = torch.Generator(device=DEV).manual_seed(N)
     qh = torch.randn(2, 3, N, d, generator=g, device=DEV).to(torch.bfloat16)
     kh = (qh.float() + 0.3 * torch.randn(2, 3, N, d, generator=g, device=DEV)).to(torch.bfloat16)
@@ -155,8 +157,6 @@ def test_merge_bit_exact(wid):
     np.testing.assert_array_equal(got, oracle.merge_target_rows(m, rows, cols))
 
 
-# R = heads * nb rows.  Up to 4096 rows one workgroup sorts them (counters in
-# LDS, the row lengths beside them while they fit); beyond, chunks of 1024
 # R = heads * nb rows in chunks of 1024: one chunk up to (931, 1); 3, 5, 10,
 # 14 and 22 chunks (the last partial) keep a key's chunk counts in registers
 # in the scan; (2048, 17) has 34 chunks and takes the two-pass scan.  Rows of
