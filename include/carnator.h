@@ -58,7 +58,9 @@
  *   calling thread.
  * - Token layout: Q, K, V and O are bf16 [B, H, N, d] with d contiguous and
  *   arbitrary element strides for B, H and N (stride_n a multiple of 8,
- *   data 16-byte aligned).  Blocks are runs of `block` consecutive tokens;
+ *   data 16-byte aligned).  The attention calls also need stride_n of Q, K
+ *   and V at most 2^24 elements (a tile's rows are addressed by 32-bit byte
+ *   offsets from the tile's first row); larger gives CARNATOR_E_UNSUPPORTED.  Blocks are runs of `block` consecutive tokens;
  *   block j covers tokens [j*block, min((j+1)*block, N)), so only the last
  *   block can be partial.  nB = ceil(N / block).  Tokens past N are never
  *   read or written.

@@ -69,6 +69,21 @@ int check_view(const carnator_view *v, const carnator_shape *s, const char *name
   return CARNATOR_OK;
 }
 
+// Q, K and V of the attention: the kernel addresses the rows of a K or V
+// tile by 32-bit byte offsets from its first row (64 rows at most).
+constexpr int64_t kMaxAttnStrideN = (int64_t)1 << 24;
+
+int check_attn_views(const carnator_view *q, const carnator_view *k, const carnator_view *v,
+                     const carnator_shape *s) {
+  int rc;
+  if ((rc = check_view(q, s, "q")) || (rc = check_view(k, s, "k")) || (rc = check_view(v, s, "v")))
+    return rc;
+  if (q->stride_n > kMaxAttnStrideN || k->stride_n > kMaxAttnStrideN || v->stride_n > kMaxAttnStrideN)
+    return fail(CARNATOR_E_UNSUPPORTED, "q, k and v stride_n must be at most %lld elements",
+                (long long)kMaxAttnStrideN);
+  return CARNATOR_OK;
+}
+
 View to_view(const carnator_view *v) {
   return View{static_cast<const uint16_t *>(v->data), v->stride_b, v->stride_h, v->stride_n};
 }
@@ -430,9 +445,7 @@ int carnator_block_sparse_attn(const carnator_view *q, const carnator_view *k,
                                hipStream_t stream) {
   int rc;
   if ((rc = check_shape(s))) return rc;
-  if ((rc = check_view(q, s, "q"))) return rc;
-  if ((rc = check_view(k, s, "k"))) return rc;
-  if ((rc = check_view(v, s, "v"))) return rc;
+  if ((rc = check_attn_views(q, k, v, s))) return rc;
   if (!out) return fail(CARNATOR_E_NULL, "out is NULL");
   if (!mask) return fail(CARNATOR_E_NULL, "mask is NULL");
   if (reinterpret_cast<uintptr_t>(out) % 16 != 0)
@@ -465,9 +478,7 @@ static int attn_lists(const carnator_view *q, const carnator_view *k, const carn
                       const int32_t *n_rows, float scale, float *lse, hipStream_t stream) {
   int rc;
   if ((rc = check_shape(s))) return rc;
-  if ((rc = check_view(q, s, "q"))) return rc;
-  if ((rc = check_view(k, s, "k"))) return rc;
-  if ((rc = check_view(v, s, "v"))) return rc;
+  if ((rc = check_attn_views(q, k, v, s))) return rc;
   if (!out) return fail(CARNATOR_E_NULL, "out is NULL");
   if (!row_ptr || !col_idx || !order) return fail(CARNATOR_E_NULL, "row_ptr, col_idx and order must be non-NULL");
   if (reinterpret_cast<uintptr_t>(out) % 16 != 0)

@@ -125,6 +125,10 @@ def test_attention_rejects_bad_arguments(L):
     assert call(n=100) == -5
     assert call(qv=_view(ptr=0)) == -1
     assert call(scale=float("inf")) == -2
+    # a row stride above 2^24 elements overflows the kernel's 32-bit tile
+    # offsets: rejected before anything is enqueued
+    assert call(qv=_view(sn=(1 << 24) + 8)) == -3
+    assert call(qv=_view(sn=1 << 24), n=100) == -5  # the largest accepted stride passes this check
 
 
 def test_attention_lists_rejects_bad_arguments(L):
@@ -142,7 +146,8 @@ def test_attention_lists_rejects_bad_arguments(L):
     assert call(osn=12) == -4
     assert call(scale=float("nan")) == -2
     assert call(shape=_shape(d=96)) == -3
-    assert "NULL" in _err(L) or _err(L)
+    assert call(qv=_view(sn=(1 << 24) + 8)) == -3
+    assert "stride_n" in _err(L)
 
 
 def test_merge_compact_signature_reject(L):
