@@ -147,7 +147,8 @@ def bank_pass(P, torch, stream, sets, flags, masks, lists, ws_mask, wl, steps):
         e[0].record(stream)
         P.build_block_mask_bits(x["q_hist"], x["k_hist"], wl.block, wl.tau, out=slots[si], workspace=ws_mask)
         e[1].record(stream)
-        P.compact_block_mask_bits(slots[si], flags[si][0], flags[si][1], trim=False, out=lb, workspace=ws_cb)
+        P.compact_block_mask_bits(slots[si], flags[si][0], flags[si][1], trim=False, out=lb, workspace=ws_cb,
+                                  attn=(wl.seq_len, wl.head_dim, wl.block))
         e[2].record(stream)
         P.pack_block_mask(masks[si], out=packed)
         e[3].record(stream)
@@ -158,7 +159,7 @@ def bank_pass(P, torch, stream, sets, flags, masks, lists, ws_mask, wl, steps):
         if i <= len(sets):
             # masks[si] holds the widened uint8 mask of this set and `lists`
             # its compaction from the last step of the per-call pass
-            P.compact_block_mask(masks[si], trim=False, out=lists)
+            P.compact_block_mask(masks[si], trim=False, out=lists, attn=(wl.seq_len, wl.head_dim, wl.block))
             nnz = int(lists[0][-1].item())
             same &= bool(torch.equal(lists[0], lb[0]) and torch.equal(lists[2], lb[2])
                          and torch.equal(lists[1][:nnz], lb[1][:nnz]))
@@ -266,7 +267,7 @@ def workload_pass(P, torch, stream, wids, steps):
             P.merge_target_rows(mask, rows, cols)
             e[3].record(stream)
             e[4].record(stream)
-            P.compact_block_mask(mask, trim=False, out=lists, workspace=ws_cmp)
+            P.compact_block_mask(mask, trim=False, out=lists, workspace=ws_cmp, attn=(N, d, bs))
             e[5].record(stream)
             e[6].record(stream)
             P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists, bs, out=o)
@@ -338,7 +339,8 @@ def region_pass(P, torch, stream, sets, wl, steps):
         e[2].record(stream)
         P.region_block_flags(region[0], wl.n_text, bs, out=flags)
         e[3].record(stream)
-        P.compact_block_mask_bits_region(slots[si], flags[0], flags[1], out=lists, workspace=ws_cb)
+        P.compact_block_mask_bits_region(slots[si], flags[0], flags[1], out=lists, workspace=ws_cb,
+                                         attn=(wl.seq_len, wl.head_dim, bs))
         e[4].record(stream)
         P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists[:3], bs, out=outs[si], n_rows=lists[3])
         e[5].record(stream)
@@ -453,7 +455,7 @@ def main():
         P.merge_target_rows(masks[si], flags[si][0], flags[si][1])
         if record == "all":
             e[2].record(stream)
-        P.compact_block_mask(masks[si], trim=False, out=lists, workspace=ws_cmp)
+        P.compact_block_mask(masks[si], trim=False, out=lists, workspace=ws_cmp, attn=(N, d, bs))
         if record:
             e[3].record(stream)
         P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists, bs, out=outs[si])

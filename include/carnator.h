@@ -86,7 +86,7 @@
 extern "C" {
 #endif
 
-#define CARNATOR_ABI_VERSION 6
+#define CARNATOR_ABI_VERSION 7
 
 typedef enum {
   CARNATOR_OK = 0,
@@ -117,6 +117,23 @@ typedef struct {
 
 /* ABI version of the loaded library (CARNATOR_ABI_VERSION). */
 int carnator_abi_version(void);
+
+/*
+ * Row order of the compaction entry points (the order in which the attention
+ * kernel runs the rows; an execution schedule the paper leaves open).  The
+ * B*H heads are cut into consecutive groups of G heads, G the most heads
+ * whose K and V (2 * seq_len * head_dim bf16 values per head) fit in 256 MiB,
+ * the size of MI355X's Infinity Cache (at least 1 head, and at least
+ * B*H / 63 heads so that there are at most 63 groups; all heads when they
+ * fit).  The order lists group 0's rows by descending list length (lower row
+ * first on equal length), then group 1's, and so on; a restricting call then
+ * lists the rows it leaves out, in ascending order.  With one group this is
+ * the plain longest-first order.  Running one group of heads at a time keeps
+ * their K and V in the Infinity Cache while they are streamed.
+ * carnator_order_group_heads returns G for a shape (0 if the shape is
+ * invalid).
+ */
+int32_t carnator_order_group_heads(const carnator_shape *shape);
 
 /* Static text of a status code (host). */
 const char *carnator_status_str(int status);
@@ -176,8 +193,9 @@ int carnator_merge_target_rows(uint8_t *mask, const carnator_shape *shape,
  *   mask      uint8 [B, H, nB, nB]
  *   row_ptr   int32 [R + 1]; row r's list is col_idx[row_ptr[r] .. row_ptr[r+1])
  *   col_idx   int32 [B*H*nB*nB] capacity; ascending key blocks per row
- *   order     int32 [R]; rows by descending list length, lower row first on
- *             equal length
+ *   order     int32 [R]; the row order above: per group of heads (one group
+ *             whenever the shape's K and V fit 256 MiB) the rows by descending
+ *             list length, lower row first on equal length
  *   workspace at least carnator_compact_block_mask_workspace_size(shape) bytes
  * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_WORKSPACE, E_HIP.
  */
@@ -380,9 +398,10 @@ int carnator_compact_block_mask_bits(const uint64_t *bits, const carnator_shape 
  * restricted to active rows and context columns,
  * M'[b,h,i,j] = M[b,h,i,j] and active_q[b,i] and context_k[b,j].
  *   bits, row_ptr, col_idx: as carnator_compact_block_mask_bits
- *   order      int32 [R]: the active rows by descending list length (lower
- *              row first on equal length), then the inactive rows in
- *              ascending order (their lists are empty)
+ *   order      int32 [R]: the active rows in the row order above (per
+ *              group of heads, by descending list length, lower row first on
+ *              equal length), then the inactive rows in ascending order
+ *              (their lists are empty)
  *   n_active   int32 [1] out (device): the number of active rows
  *   workspace  carnator_compact_block_mask_bits_workspace_size(shape) bytes
  * Errors: E_NULL, E_SHAPE, E_UNSUPPORTED, E_ALIGN, E_WORKSPACE, E_HIP.
@@ -456,8 +475,9 @@ int carnator_block_sparse_attn(const carnator_view *q, const carnator_view *k,
  *
  *   q, k, v, out, out strides, shape, scale, lse: as carnator_block_sparse_attn
  *   row_ptr  int32 [R + 1], col_idx int32 (row lists, ascending), order
- *            int32 [R] (a permutation of the R = B*H*nB rows, longest list
- *            first): exactly as written by carnator_compact_block_mask
+ *            int32 [R] (a permutation of the R = B*H*nB rows, the row order
+ *            above): as written by carnator_compact_block_mask (any
+ *            permutation gives the same output; the order sets the speed)
  * The kernel clamps rows, list bounds and block indices into range, so
  * malformed lists give wrong output but no access outside q, k, v, out,
  * lse and the lists' documented extents.

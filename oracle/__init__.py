@@ -42,7 +42,7 @@ Readings taken where the paper is silent are listed in the module docstrings
 of each submodule.
 """
 from .mask import (pool_blocks, block_scores, select_row, build_block_mask,
-                   merge_target_rows, compact_mask, row_admissible_masks, TIE_EPS,
+                   merge_target_rows, compact_mask, group_rows_order, row_admissible_masks, TIE_EPS,
                    FRAGILE_EPS, pack_mask, unpack_mask)
 from .attention import block_sparse_attention, token_mask_from_blocks
 from .gate import (ciede2000, support_area, normalized_shape, d_size, d_shape, gate, first_compatible,
@@ -55,7 +55,7 @@ from .convert import to_f64
 
 __all__ = [
     "pool_blocks", "block_scores", "select_row", "build_block_mask",
-    "merge_target_rows", "compact_mask", "row_admissible_masks", "TIE_EPS",
+    "merge_target_rows", "compact_mask", "group_rows_order", "row_admissible_masks", "TIE_EPS",
     "FRAGILE_EPS", "pack_mask", "unpack_mask", "block_sparse_attention", "token_mask_from_blocks",
     "cosine_similarity", "topk_cosine", "to_f64",
     "dilate_frames", "chebyshev_distance", "smoothstep", "regions", "latent_fusion",

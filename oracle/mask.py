@@ -152,13 +152,28 @@ def merge_target_rows(mask: np.ndarray, row_flags: np.ndarray, col_flags: np.nda
     return out.astype(np.uint8)
 
 
-def compact_mask(mask: np.ndarray):
+def group_rows_order(order: np.ndarray, group_rows: int) -> np.ndarray:
+    """The row order taken apart by head group, each group keeping its order.
+
+    Rows are (b, h, i) in row-major order, so heads [g G, (g + 1) G) are the
+    rows [g group_rows, (g + 1) group_rows), group_rows = G nB.  The result
+    lists group 0's rows in the order they have in ``order``, then group 1's,
+    and so on (an execution schedule; the paper does not fix one).
+    """
+    order = np.asarray(order)
+    if group_rows is None or order.size == 0:
+        return order
+    return order[np.argsort(order // int(group_rows), kind="stable")]
+
+
+def compact_mask(mask: np.ndarray, group_heads: int = None):
     """Per-row list of kept key blocks.
 
     Rows are (b, h, i) in row-major order.  Returns ``row_ptr`` (int32
     [R+1]), ``col_idx`` (int32 [nnz], ascending within a row) and ``order``
     (int32 [R]: rows by descending list length, lower row first on equal
-    length).
+    length; with ``group_heads`` G, that order per group of G consecutive
+    heads, group after group).
     """
     m = (np.asarray(mask) != 0)
     nb = m.shape[-1]
@@ -168,6 +183,8 @@ def compact_mask(mask: np.ndarray):
     row_ptr[1:] = np.cumsum(counts)
     col_idx = np.nonzero(flat)[1]
     order = np.argsort(-counts, kind="stable")
+    if group_heads is not None:
+        order = group_rows_order(order, int(group_heads) * nb)
     return row_ptr.astype(np.int32), col_idx.astype(np.int32), order.astype(np.int32)
 
 

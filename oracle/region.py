@@ -37,6 +37,8 @@ Readings (the paper is silent on these points):
 """
 import numpy as np
 
+from .mask import group_rows_order
+
 EVIDENCE, BAND, CONTEXT, OUTSIDE = 3, 2, 1, 0
 
 
@@ -132,12 +134,15 @@ def restrict_mask(mask: np.ndarray, active_q: np.ndarray, context_k: np.ndarray)
     return (m & a & c).astype(np.uint8)
 
 
-def compact_restricted(mask: np.ndarray, active_q: np.ndarray, context_k: np.ndarray):
+def compact_restricted(mask: np.ndarray, active_q: np.ndarray, context_k: np.ndarray,
+                       group_heads: int = None):
     """Lists of the restricted mask: (row_ptr, col_idx, order, n_active).
 
     Rows are (b, h, i) in row-major order; order lists the active rows by
-    descending length (lower row first on equal length), then the inactive
-    rows in ascending order; n_active is the number of active rows."""
+    descending length (lower row first on equal length; with ``group_heads``
+    G, that order per group of G consecutive heads, group after group), then
+    the inactive rows in ascending order; n_active is the number of active
+    rows."""
     m = restrict_mask(mask, active_q, context_k)
     B, H, nb, _ = m.shape
     flat = m.reshape(-1, nb)
@@ -149,5 +154,7 @@ def compact_restricted(mask: np.ndarray, active_q: np.ndarray, context_k: np.nda
     rows = np.arange(flat.shape[0])
     act = rows[row_active]
     act = act[np.argsort(-counts[act], kind="stable")]
+    if group_heads is not None:
+        act = group_rows_order(act, int(group_heads) * nb)
     order = np.concatenate([act, rows[~row_active]])
     return (row_ptr.astype(np.int32), col_idx.astype(np.int32), order.astype(np.int32), int(act.size))

@@ -19,13 +19,13 @@ LIB_PATH = os.path.join(_PKG, "libcarnator.so")
 
 CARNATOR_OK = 0
 # CARNATOR_ABI_VERSION of include/carnator.h this binding marshals for
-ABI_VERSION = 6
+ABI_VERSION = 7
 STATUS = {0: "OK", -1: "E_NULL", -2: "E_SHAPE", -3: "E_UNSUPPORTED", -4: "E_ALIGN",
           -5: "E_WORKSPACE", -6: "E_HIP"}
 
 # Every entry point declared in include/carnator.h.
 EXPORTS = (
-    "carnator_abi_version", "carnator_status_str", "carnator_last_error",
+    "carnator_abi_version", "carnator_status_str", "carnator_last_error", "carnator_order_group_heads",
     "carnator_build_block_mask_workspace_size", "carnator_build_block_mask",
     "carnator_merge_target_rows",
     "carnator_block_mass_exact_workspace_size", "carnator_block_mass_exact", "carnator_select_block_mask",
@@ -74,6 +74,7 @@ def lib() -> ctypes.CDLL:
         SP, VP = ctypes.POINTER(Shape), ctypes.POINTER(View)
         sig = {
             "carnator_abi_version": (ctypes.c_int, []),
+            "carnator_order_group_heads": (ctypes.c_int32, [ctypes.POINTER(Shape)]),
             "carnator_status_str": (ctypes.c_char_p, [ctypes.c_int]),
             "carnator_last_error": (ctypes.c_char_p, []),
             "carnator_build_block_mask_workspace_size": (SZ, [SP]),
@@ -137,6 +138,30 @@ def _ptr(t: Optional[torch.Tensor]):
 def _shape(t: torch.Tensor, block: int) -> Shape:
     B, H, N, d = t.shape
     return Shape(B, H, N, d, block)
+
+
+def _mask_shape(B: int, H: int, nb: int, attn=None) -> Shape:
+    """Shape of a call on block masks alone.  ``attn`` = (seq_len, head_dim,
+    block) of the attention the lists serve sets the head groups of the row
+    order (order_group_heads); without it the shape is seq_len nb * 64,
+    head_dim 64, block 64."""
+    if attn is None:
+        return Shape(B, H, nb * 64, 64, 64)
+    N, d, bs = (int(x) for x in attn)
+    if -(-N // bs) != nb:
+        raise ValueError("attn (seq_len %d, block %d) gives %d blocks, the mask has %d" % (N, bs, -(-N // bs), nb))
+    return Shape(B, H, N, d, bs)
+
+
+def order_group_heads(batch: int, heads: int, nb: int, attn=None) -> int:
+    """Heads per group of the row order the compaction calls write for masks
+    [batch, heads, nb, nb] (carnator_order_group_heads; ``attn`` as in the
+    compaction calls)."""
+    s = _mask_shape(batch, heads, nb, attn)
+    g = lib().carnator_order_group_heads(ctypes.byref(s))
+    if g <= 0:
+        raise ValueError("invalid shape")
+    return int(g)
 
 
 def _view(t: torch.Tensor) -> View:
@@ -250,16 +275,18 @@ def compact_block_mask_workspace(mask: torch.Tensor) -> torch.Tensor:
 
 
 def compact_block_mask(mask: torch.Tensor, trim: bool = True, out=None,
-                       workspace: Optional[torch.Tensor] = None):
+                       workspace: Optional[torch.Tensor] = None, attn=None):
     """(row_ptr int32 [R+1], col_idx int32, order int32 [R]).
 
     With trim (the default) the stream is synchronised once to cut col_idx to
     its nnz entries; trim=False keeps the full B*H*nB*nB capacity and does not
     synchronise.  ``out`` may pass preallocated (row_ptr, col_idx, order).
+    ``attn`` = (seq_len, head_dim, block) of the attention the lists serve: it
+    sets the head groups of the order (see order_group_heads).
     """
     B, H, nb, _ = mask.shape
     R = B * H * nb
-    s = Shape(B, H, nb * 64, 64, 64)
+    s = _mask_shape(B, H, nb, attn)
     dev = mask.device
     if not mask.is_contiguous() or mask.dtype != torch.uint8:
         raise ValueError("mask must be contiguous uint8 [B, H, nB, nB]")
@@ -358,16 +385,16 @@ def compact_block_mask_bits_workspace(bits: torch.Tensor) -> torch.Tensor:
 
 
 def compact_block_mask_bits(bits: torch.Tensor, target_rows=None, dense_cols=None, trim: bool = True,
-                            out=None, workspace: Optional[torch.Tensor] = None):
+                            out=None, workspace: Optional[torch.Tensor] = None, attn=None):
     """(row_ptr, col_idx, order) of the packed mask widened by target_rows and
-    dense_cols (each [B, nB] or None); the bits are not modified.  trim and out
-    as in compact_block_mask."""
+    dense_cols (each [B, nB] or None); the bits are not modified.  trim, out
+    and attn as in compact_block_mask."""
     B, H, nb = _bits_shape(bits)
     R = B * H * nb
     dev = bits.device
     rows = _dev_u8(target_rows, dev, (B, nb))
     cols = _dev_u8(dense_cols, dev, (B, nb))
-    s = Shape(B, H, nb * 64, 64, 64)
+    s = _mask_shape(B, H, nb, attn)
     if out is None:
         out = (torch.empty(R + 1, dtype=torch.int32, device=dev),
                torch.empty(max(R * nb, 1), dtype=torch.int32, device=dev),
@@ -416,10 +443,11 @@ class MaskBank:
         return pack_block_mask(mask, out=self.slot(step, branch, layer))
 
     def lists(self, step: int, branch: int, layer: int, target_rows=None, dense_cols=None,
-              trim: bool = True, out=None, workspace: Optional[torch.Tensor] = None):
-        """Compacted lists of one slot for a target (compact_block_mask_bits)."""
+              trim: bool = True, out=None, workspace: Optional[torch.Tensor] = None, attn=None):
+        """Compacted lists of one slot for a target (compact_block_mask_bits;
+        attn as there)."""
         return compact_block_mask_bits(self.slot(step, branch, layer), target_rows, dense_cols, trim=trim,
-                                       out=out, workspace=workspace)
+                                       out=out, workspace=workspace, attn=attn)
 
 
 def block_sparse_attn_workspace(q: torch.Tensor, block: int) -> torch.Tensor:
@@ -558,17 +586,18 @@ def region_block_flags(region: torch.Tensor, n_text: int, block: int, out=None):
 
 
 def compact_block_mask_bits_region(bits: torch.Tensor, active_q, context_k, out=None,
-                                   workspace: Optional[torch.Tensor] = None):
+                                   workspace: Optional[torch.Tensor] = None, attn=None):
     """(row_ptr, col_idx, order, n_active) of the packed mask restricted to
     active rows and context columns (carnator_compact_block_mask_bits_region).
     col_idx keeps its full capacity and n_active stays on the device (an int32
-    tensor of one element), so nothing synchronises."""
+    tensor of one element), so nothing synchronises.  attn as in
+    compact_block_mask."""
     B, H, nb = _bits_shape(bits)
     R = B * H * nb
     dev = bits.device
     act = _dev_u8(active_q, dev, (B, nb))
     ctx = _dev_u8(context_k, dev, (B, nb))
-    s = Shape(B, H, nb * 64, 64, 64)
+    s = _mask_shape(B, H, nb, attn)
     if out is None:
         out = (torch.empty(R + 1, dtype=torch.int32, device=dev),
                torch.empty(max(R * nb, 1), dtype=torch.int32, device=dev),

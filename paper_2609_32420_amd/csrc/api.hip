@@ -58,6 +58,11 @@ int check_shape(const carnator_shape *s) {
 
 int n_blocks(const carnator_shape *s) { return (s->seq_len + s->block - 1) / s->block; }
 
+// Rows per head group of the row order (a valid shape).
+int64_t group_rows(const carnator_shape *s) {
+  return (int64_t)order_group_heads(s->batch * s->heads, s->seq_len, s->head_dim) * n_blocks(s);
+}
+
 int check_view(const carnator_view *v, const carnator_shape *s, const char *name) {
   if (!v || !v->data) return fail(CARNATOR_E_NULL, "%s is NULL", name);
   if (reinterpret_cast<uintptr_t>(v->data) % 16 != 0)
@@ -123,6 +128,11 @@ AttnWs attn_layout(const carnator_shape *s) {
 extern "C" {
 
 int carnator_abi_version(void) { return CARNATOR_ABI_VERSION; }
+
+int32_t carnator_order_group_heads(const carnator_shape *s) {
+  if (!s || check_shape(s) != CARNATOR_OK) return 0;
+  return order_group_heads(s->batch * s->heads, s->seq_len, s->head_dim);
+}
 
 const char *carnator_status_str(int status) {
   switch (status) {
@@ -283,7 +293,7 @@ int carnator_compact_block_mask(const uint8_t *mask, const carnator_shape *s, in
     return fail(CARNATOR_E_NULL, "mask, row_ptr, col_idx and order must be non-NULL");
   if ((rc = check_ws(workspace, ws_bytes, carnator_compact_block_mask_workspace_size(s)))) return rc;
   const int nB = n_blocks(s);
-  hipError_t e = launch_compact(mask, (int64_t)s->batch * s->heads * nB, nB, row_ptr, col_idx,
+  hipError_t e = launch_compact(mask, (int64_t)s->batch * s->heads * nB, nB, group_rows(s), row_ptr, col_idx,
                                 order, workspace, stream);
   if (e != hipSuccess) return hip_fail(e, "compact");
   return ok();
@@ -335,7 +345,7 @@ int carnator_compact_block_mask_bits(const uint64_t *bits, const carnator_shape 
     return fail(CARNATOR_E_ALIGN, "bits must be 8-byte aligned");
   if ((rc = check_ws(workspace, ws_bytes, carnator_compact_block_mask_bits_workspace_size(s))))
     return rc;
-  hipError_t e = launch_compact_bits(bits, s->batch, s->heads, n_blocks(s), target_rows,
+  hipError_t e = launch_compact_bits(bits, s->batch, s->heads, n_blocks(s), group_rows(s), target_rows,
                                      dense_cols, false, row_ptr, col_idx, order, nullptr, workspace,
                                      stream);
   if (e != hipSuccess) return hip_fail(e, "compact_bits");
@@ -425,7 +435,7 @@ int carnator_compact_block_mask_bits_region(const uint64_t *bits, const carnator
     return fail(CARNATOR_E_ALIGN, "bits must be 8-byte aligned");
   if ((rc = check_ws(workspace, ws_bytes, carnator_compact_block_mask_bits_workspace_size(s))))
     return rc;
-  hipError_t e = launch_compact_bits(bits, s->batch, s->heads, n_blocks(s), active_q, context_k,
+  hipError_t e = launch_compact_bits(bits, s->batch, s->heads, n_blocks(s), group_rows(s), active_q, context_k,
                                      true, row_ptr, col_idx, order, n_active, workspace, stream);
   if (e != hipSuccess) return hip_fail(e, "compact_bits_region");
   return ok();
@@ -461,7 +471,7 @@ int carnator_block_sparse_attn(const carnator_view *q, const carnator_view *k,
   int32_t *order = reinterpret_cast<int32_t *>(ws + L.order);
   const int nB = n_blocks(s);
   const float sc = scale > 0.f ? scale : (float)(1.0 / sqrt((double)s->head_dim));
-  hipError_t e = launch_compact(mask, (int64_t)s->batch * s->heads * nB, nB, row_ptr, col_idx,
+  hipError_t e = launch_compact(mask, (int64_t)s->batch * s->heads * nB, nB, group_rows(s), row_ptr, col_idx,
                                 order, ws + L.scratch, stream);
   if (e != hipSuccess) return hip_fail(e, "compact");
   e = launch_bsattn(to_view(q), to_view(k), to_view(v), static_cast<uint16_t *>(out), osb, osh, osn,

@@ -23,6 +23,32 @@ namespace {
 // Rows per chunk of the row sort (one thread per row of a chunk).
 constexpr int kChunk = 1024;
 
+// Rows in head groups of gr rows (gr a multiple of nB; one group when
+// gr >= R), each group cut into chunks of kChunk rows: chunk c is chunk
+// c mod cpg of group c / cpg, cpg = ceil(gr / kChunk), so no chunk spans two
+// groups (the last chunk of a group, and chunks past R, may be partial or
+// empty).
+struct Chunks {
+  int64_t R, gr;
+  int cpg;
+  __host__ __device__ int64_t lo(int c) const {
+    const int g = c / cpg;
+    const int64_t r = (int64_t)g * gr + (int64_t)(c - g * cpg) * kChunk;
+    return r < R ? r : R;
+  }
+  __host__ __device__ int64_t hi(int c) const {
+    const int g = c / cpg;
+    int64_t r = (int64_t)g * gr + (int64_t)(c - g * cpg + 1) * kChunk;
+    const int64_t ge = (int64_t)(g + 1) * gr;
+    r = r < ge ? r : ge;
+    return r < R ? r : R;
+  }
+  __host__ __device__ int of(int64_t r) const {
+    const int64_t g = r / gr;
+    return (int)(g * cpg + (r - g * gr) / kChunk);
+  }
+};
+
 // One thread per mask byte.
 __global__ void __launch_bounds__(256) merge_kernel(uint8_t *__restrict__ mask, int H, int nB,
                                                     int64_t total,
@@ -164,6 +190,7 @@ struct FillBits {
   const uint64_t *colw;
   bool narrow;
   const int32_t *coff, *rloc;
+  Chunks ch;
   int32_t *col_idx;
   __device__ void operator()(int64_t r, int lane, int *) const {
     if (r >= R || !row_kept((int)r, nB, HnB, rows, narrow)) return;
@@ -171,7 +198,7 @@ struct FillBits {
     const uint64_t mine =
         lane < nw ? merged_word(bits, (int)r, lane, nB, nw, HnB, rows, colw, narrow) : 0ull;
     const uint64_t below = (1ull << lane) - 1ull;
-    int pos = coff[r / kChunk] + rloc[r];
+    int pos = coff[ch.of(r)] + rloc[r];
     for (int c = 0; c < nw; ++c) {
       const uint64_t w = read_lane(mine, c);
       if ((w >> lane) & 1ull) col_idx[pos + __popcll(w & below)] = c * 64 + lane;
@@ -284,13 +311,14 @@ struct FillBytes {
   int64_t R;
   int nB;
   const int32_t *coff, *rloc;
+  Chunks ch;
   int32_t *col_idx;
   __device__ void operator()(int64_t r, int lane, int *stage) const {
     if (r >= R) return;
     uint32_t keep[NU];
     int col0[NU];
     load_row16<NU>(mask + r * nB, nB, lane, keep, col0);
-    const int pos = coff[r / kChunk] + rloc[r];
+    const int pos = coff[ch.of(r)] + rloc[r];
     int n = 0;
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
@@ -305,20 +333,26 @@ struct FillBytes {
   }
 };
 
-// ---- row_ptr and the order of rows by descending list length
+// ---- row_ptr and the order of rows
 //
 // Sort key of a row: nB - length, so that longer lists come first, and
 // nB + 1 for a row a restriction leaves out (length -1: an empty list,
-// placed after every other row).  Rows come in G chunks of kChunk rows.
-//   sort_hist_kernel, one workgroup per chunk g: the chunk's key histogram
-//     to hist[g K + key] (K = nB + 2), each row's exclusive prefix of the
-//     lengths inside the chunk to rloc, the chunk's length sum to csum[g];
-//   sort_scan_kernel, one workgroup: for each key, the exclusive prefix of
-//     its counts over the chunks plus the exclusive prefix of the key totals
-//     (key order) -- the first slot in order of chunk g's rows of each key,
-//     in place of hist -- the exclusive scan of csum in place (the chunk
-//     offsets of row_ptr), row_ptr[R] and *n_active (the first slot of key
-//     nB + 1: the number of rows not left out);
+// placed after every other row).  The order lists the rows group by group
+// (the Chunks groups of heads; one group when they all fit), each group's
+// rows by key, lower row first on equal key, then the rows left out in row
+// order.
+//   sort_hist_kernel, one workgroup per chunk c: the chunk's key histogram
+//     to hist[c K + key] (K = nB + 2), each row's exclusive prefix of the
+//     lengths inside the chunk to rloc, the chunk's length sum to csum[c];
+//   sort_scan_kernel, one workgroup, thread t owning keys t, t + 1024, ...:
+//     for each active key the exclusive prefix of its counts over the chunks
+//     of each group and the group's total of that key (gtot[g (nB + 1) +
+//     key]); for the left-out key the prefix over all chunks.  The totals,
+//     scanned in (group, key) order, give the first slot of each group's
+//     rows of each key and are added to the prefixes: hist[c K + key] is
+//     then the first slot in order of chunk c's rows of that key (the
+//     left-out rows start after all active ones).  csum in place: the chunk
+//     offsets of row_ptr; row_ptr[R]; *n_active, the number of active rows;
 //   place_fill_kernel, workgroups 0 .. G - 1, one per chunk: row_ptr of its
 //     rows (chunk offset plus rloc), and each row's slot in order: its
 //     chunk's first slot for its key, plus the rows of that key in earlier
@@ -334,86 +368,111 @@ constexpr int kSortWaves = kScanThreads / 64;
 __device__ inline int sort_key(int L, int nB) { return L < 0 ? nB + 1 : nB - L; }
 
 __global__ void __launch_bounds__(kScanThreads) sort_hist_kernel(const int32_t *__restrict__ len,
-                                                                 int R, int nB,
+                                                                 Chunks ch, int nB,
                                                                  int32_t *__restrict__ hist,
                                                                  int32_t *__restrict__ csum,
                                                                  int32_t *__restrict__ rloc) {
   extern __shared__ int hk[];  // nB + 2 counters
   __shared__ int sh[kSortWaves];
-  const int g = blockIdx.x, t = threadIdx.x;
+  const int c = blockIdx.x, t = threadIdx.x;
   const int K = nB + 2;
   for (int k = t; k < K; k += kScanThreads) hk[k] = 0;
   __syncthreads();
-  const int r = g * kChunk + t;
-  const int L = r < R ? len[r] : 0;
-  if (r < R) atomicAdd(&hk[sort_key(L, nB)], 1);
+  const int64_t r = ch.lo(c) + t;
+  const bool on = r < ch.hi(c);
+  const int L = on ? len[r] : 0;
+  if (on) atomicAdd(&hk[sort_key(L, nB)], 1);
   int total;
   const int ex = block_excl_scan(max(L, 0), sh, &total);  // ends with a barrier
-  if (r < R) rloc[r] = ex;
-  for (int k = t; k < K; k += kScanThreads) hist[(int64_t)g * K + k] = hk[k];
-  if (t == 0) csum[g] = total;
+  if (on) rloc[r] = ex;
+  for (int k = t; k < K; k += kScanThreads) hist[(int64_t)c * K + k] = hk[k];
+  if (t == 0) csum[c] = total;
 }
 
-// One workgroup, thread t owning keys t, t + 1024, t + 2048: the chunk
-// counts of each of its keys (coalesced over the threads), the key totals
-// scanned in key order one pass of 1024 keys at a time, and each count
-// replaced by the key's first slot in that chunk.  Up to 32 chunks
-// the counts stay in registers (one round trip; REGS >= G, the smallest of
-// 4, 8, 16, 32); beyond, they are rewritten as prefixes sixteen loads at a
-// time and the key offset added in a second pass.  Then the chunk offsets.
+// Up to REGS chunks a key's counts stay in registers (one round trip; REGS
+// >= G, the smallest of 4, 8, 16, 32); beyond, they are read sixteen at a
+// time.
 template <int REGS>
-__global__ void __launch_bounds__(kScanThreads) sort_scan_kernel(int R, int nB, int G,
+__global__ void __launch_bounds__(kScanThreads) sort_scan_kernel(int R, int nB, int G, int cpg,
+                                                                 int ngroups,
                                                                  int32_t *__restrict__ hist,
                                                                  int32_t *__restrict__ csum,
+                                                                 int32_t *__restrict__ gtot,
                                                                  int32_t *__restrict__ row_ptr,
                                                                  int32_t *__restrict__ n_active) {
   __shared__ int sh[kSortWaves];
   const int t = threadIdx.x;
-  const int K = nB + 2;
-  int carry = 0;
-  for (int k0 = 0; k0 < K; k0 += kScanThreads) {
-    const int k = k0 + t;
+  const int K = nB + 2, KA = nB + 1;
+  // in-group prefixes (a key's running count restarts at each group's first
+  // chunk; the left-out key's does not) and the group totals
+  for (int k = t; k < K; k += kScanThreads) {
+    const bool left_out = k == KA;
+    int run = 0;
+    auto step = [&](int c, int v) __attribute__((always_inline)) {
+      if (!left_out && c % cpg == 0 && c > 0) {
+        gtot[(int64_t)(c / cpg - 1) * KA + k] = run;
+        run = 0;
+      }
+      hist[(int64_t)c * K + k] = run;
+      run += v;
+    };
     if (G <= REGS) {
-      // every chunk count of the key in registers, all loads in flight
       int v[REGS];
 #pragma unroll
-      for (int u = 0; u < REGS; ++u) v[u] = (k < K && u < G) ? hist[(int64_t)u * K + k] : 0;
-      int tot = 0;
+      for (int u = 0; u < REGS; ++u) v[u] = u < G ? hist[(int64_t)u * K + k] : 0;
 #pragma unroll
-      for (int u = 0; u < REGS; ++u) tot += v[u];
-      int all;
-      int run = block_excl_scan(tot, sh, &all) + carry;
-      carry += all;
-      if (k < K) {
-#pragma unroll
-        for (int u = 0; u < REGS; ++u) {
-          if (u < G) hist[(int64_t)u * K + k] = run;
-          run += v[u];
-        }
-      }
-      continue;
-    }
-    int tot = 0;
-    if (k < K) {
-      for (int g0 = 0; g0 < G; g0 += 16) {
+      for (int u = 0; u < REGS; ++u)
+        if (u < G) step(u, v[u]);
+    } else {
+      for (int c0 = 0; c0 < G; c0 += 16) {
         int v[16];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = g0 + u < G ? hist[(int64_t)(g0 + u) * K + k] : 0;
+        for (int u = 0; u < 16; ++u) v[u] = c0 + u < G ? hist[(int64_t)(c0 + u) * K + k] : 0;
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          if (g0 + u < G) hist[(int64_t)(g0 + u) * K + k] = tot;
-          tot += v[u];
-        }
+        for (int u = 0; u < 16; ++u)
+          if (c0 + u < G) step(c0 + u, v[u]);
       }
     }
-    int all;
-    const int ex = block_excl_scan(tot, sh, &all) + carry;
-    carry += all;
-    if (k < K) {
-      for (int g = 0; g < G; ++g) hist[(int64_t)g * K + k] += ex;
+    if (!left_out) gtot[(int64_t)(ngroups - 1) * KA + k] = run;
+  }
+  __threadfence_block();  // gtot, written and then read by other threads of the workgroup
+  __syncthreads();
+  // the group totals scanned in (group, key) order, a contiguous run of
+  // entries per thread
+  int active;
+  {
+    const int64_t M = (int64_t)ngroups * KA;
+    const int64_t per = (M + kScanThreads - 1) / kScanThreads;
+    const int64_t lo = min(M, per * t), hi = min(M, lo + per);
+    int local = 0;
+    for (int64_t i = lo; i < hi; ++i) local += gtot[i];
+    int run = block_excl_scan(local, sh, &active);  // ends with a barrier
+    for (int64_t i = lo; i < hi; ++i) {
+      const int c = gtot[i];
+      gtot[i] = run;
+      run += c;
     }
   }
-  // chunk offsets of row_ptr
+  __threadfence_block();
+  __syncthreads();
+  // first slots: prefix + the group's start for the key (the active rows'
+  // count for the left-out key)
+  for (int k = t; k < K; k += kScanThreads) {
+    const bool left_out = k == KA;
+    for (int c0 = 0; c0 < G; c0 += 8) {
+      int add[8], v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int c = c0 + u;
+        add[u] = c < G ? (left_out ? active : gtot[(int64_t)(c / cpg) * KA + k]) : 0;
+        v[u] = c < G ? hist[(int64_t)c * K + k] : 0;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (c0 + u < G) hist[(int64_t)(c0 + u) * K + k] = v[u] + add[u];
+    }
+  }
+  // chunk offsets of row_ptr (the chunks are in row order)
   int rcarry = 0;
   for (int g0 = 0; g0 < G; g0 += kScanThreads) {
     const int g = g0 + t;
@@ -423,17 +482,100 @@ __global__ void __launch_bounds__(kScanThreads) sort_scan_kernel(int R, int nB, 
     if (g < G) csum[g] = rcarry + ex;
     rcarry += tot;
   }
-  if (t == 0) row_ptr[R] = rcarry;
-  // the first slot of key nB + 1 (chunk 0): written by the thread owning it
-  if (n_active != nullptr && t == (nB + 1) % kScanThreads) {
-    __threadfence_block();
-    *n_active = hist[nB + 1];
+  if (t == 0) {
+    row_ptr[R] = rcarry;
+    if (n_active != nullptr) *n_active = active;
+  }
+}
+
+// The same when every key has a thread (nB + 2 <= 1024), a key's counts fit
+// REGS registers (G <= REGS) and the group totals fit the LDS.  The counts
+// are read once and each first slot written once.  The group totals sit in
+// LDS as [group][active key] followed by [group] of the left-out key, so one
+// exclusive scan in that order yields every group's start for every key (the
+// left-out key's after all active rows), and a key's running count restarts
+// at each group's first chunk for every key alike.
+template <int REGS>
+__global__ void __launch_bounds__(kScanThreads) sort_scan_fast_kernel(int R, int nB, int G, int cpg,
+                                                                      int ngroups,
+                                                                      int32_t *__restrict__ hist,
+                                                                      int32_t *__restrict__ csum,
+                                                                      int32_t *__restrict__ row_ptr,
+                                                                      int32_t *__restrict__ n_active) {
+  extern __shared__ int gt[];  // [ngroups][nB + 1], then [ngroups]
+  __shared__ int sh[kSortWaves];
+  const int t = threadIdx.x;
+  const int K = nB + 2, KA = nB + 1;
+  const int M = ngroups * KA;
+  const bool on = t < K;
+  // a key's total of group g at gt[slot0 + g * gstride]
+  const int slot0 = t == KA ? M : t, gstride = t == KA ? 1 : KA;
+  int pre[REGS];
+  if (on) {
+    int v[REGS];
+#pragma unroll
+    for (int u = 0; u < REGS; ++u) {  // branch-free: chunk G - 1 again past the last
+      const int x = hist[(int64_t)min(u, G - 1) * K + t];
+      v[u] = u < G ? x : 0;
+    }
+    int run = 0, j = 0, g = 0;
+#pragma unroll
+    for (int u = 0; u < REGS; ++u) {
+      if (j == cpg && u < G) {
+        gt[slot0 + g * gstride] = run;
+        run = 0, j = 0, ++g;
+      }
+      pre[u] = run;
+      run += v[u];
+      ++j;
+    }
+    gt[slot0 + g * gstride] = run;
+  }
+  __syncthreads();
+  {
+    const int n = M + ngroups;
+    const int per = (n + kScanThreads - 1) / kScanThreads;
+    const int lo = min(n, per * t), hi = min(n, lo + per);
+    int local = 0;
+    for (int i = lo; i < hi; ++i) local += gt[i];
+    int total;
+    int run = block_excl_scan(local, sh, &total);  // ends with a barrier
+    for (int i = lo; i < hi; ++i) {
+      const int c = gt[i];
+      gt[i] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+  if (on) {
+    int j = 0, g = 0;
+#pragma unroll
+    for (int u = 0; u < REGS; ++u) {
+      if (u < G) {
+        if (j == cpg) j = 0, ++g;
+        hist[(int64_t)u * K + t] = pre[u] + gt[slot0 + g * gstride];
+        ++j;
+      }
+    }
+  }
+  int rcarry = 0;
+  for (int g0 = 0; g0 < G; g0 += kScanThreads) {
+    const int g = g0 + t;
+    const int x = g < G ? csum[g] : 0;
+    int tot;
+    const int ex = block_excl_scan(x, sh, &tot);
+    if (g < G) csum[g] = rcarry + ex;
+    rcarry += tot;
+  }
+  if (t == 0) {
+    row_ptr[R] = rcarry;
+    if (n_active != nullptr) *n_active = gt[M];  // the left-out rows' start: all active rows
   }
 }
 
 template <class Fill>
 __global__ void __launch_bounds__(kScanThreads) place_fill_kernel(const int32_t *__restrict__ len,
-                                                                  int R, int nB, int G,
+                                                                  Chunks ch, int nB, int G,
                                                                   const int32_t *__restrict__ base,
                                                                   const int32_t *__restrict__ coff,
                                                                   const int32_t *__restrict__ rloc,
@@ -449,24 +591,24 @@ __global__ void __launch_bounds__(kScanThreads) place_fill_kernel(const int32_t 
     fill(((int64_t)blockIdx.x - G) * kSortWaves + w, lane, wc + w * K);
     return;
   }
-  const int g = blockIdx.x;
+  const int c = blockIdx.x;
   for (int i = t; i < K * kSortWaves; i += kScanThreads) wc[i] = 0;
   __syncthreads();
-  const int r = g * kChunk + t;
-  const bool on = r < R;
+  const int64_t r = ch.lo(c) + t;
+  const bool on = r < ch.hi(c);
   const int key = on ? sort_key(len[r], nB) : 0;
   if (on) {
     atomicAdd(&wc[key * kSortWaves + w], 1);
-    row_ptr[r] = coff[g] + rloc[r];
+    row_ptr[r] = coff[c] + rloc[r];
   }
   __syncthreads();
   for (int k = t; k < K; k += kScanThreads) {
-    int run = base[(int64_t)g * K + k];
+    int run = base[(int64_t)c * K + k];
 #pragma unroll
     for (int q = 0; q < kSortWaves; ++q) {
-      const int c = wc[k * kSortWaves + q];
+      const int n = wc[k * kSortWaves + q];
       wc[k * kSortWaves + q] = run;
-      run += c;
+      run += n;
     }
   }
   __syncthreads();
@@ -477,7 +619,7 @@ __global__ void __launch_bounds__(kScanThreads) place_fill_kernel(const int32_t 
     const unsigned long long ones = __ballot(on && ((key >> b) & 1));
     m &= ((key >> b) & 1) ? ones : ~ones;
   }
-  if (on) order[wc[key * kSortWaves + w] + __popcll(m & ((1ull << lane) - 1ull))] = r;
+  if (on) order[wc[key * kSortWaves + w] + __popcll(m & ((1ull << lane) - 1ull))] = (int32_t)r;
 }
 
 }  // namespace
@@ -490,53 +632,96 @@ hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows
   return hipGetLastError();
 }
 
-static int sort_chunks(int64_t R) { return (int)((R + kChunk - 1) / kChunk); }
+int order_group_heads(int heads, int64_t N, int d) {
+  const int64_t per = 2 * N * d * (int64_t)sizeof(uint16_t);  // K and V of one head
+  int64_t g = per > 0 ? kOrderGroupBytes / per : heads;
+  const int64_t least = (heads + 62) / 63;  // at most 63 groups
+  g = g < 1 ? 1 : g;
+  g = g < least ? least : g;
+  return g >= heads ? heads : (int)g;
+}
+
+// The chunks of R rows in groups of group_rows (>= R or <= 0: one group).
+static Chunks make_chunks(int64_t R, int64_t group_rows) {
+  const int64_t gr = (group_rows <= 0 || group_rows >= R) ? (R > 0 ? R : 1) : group_rows;
+  return Chunks{R, gr, (int)((gr + kChunk - 1) / kChunk)};
+}
+static int n_groups(const Chunks &ch) { return (int)((ch.R + ch.gr - 1) / ch.gr); }
+
+// LDS of the single-pass scan's group totals.
+constexpr size_t kScanFastLds = 128 * 1024;
+
+// At most 63 groups, each adding at most one partial chunk (the launch counts
+// the last group's chunks only as far as its rows reach).
+static int64_t max_chunks(int64_t R) { return (R + kChunk - 1) / kChunk + 63; }
 
 // The list lengths, then the chunk histograms (key offsets after the scan),
-// the chunk length sums (chunk offsets after the scan) and the in-chunk
-// prefixes of the lengths.
+// the chunk length sums (chunk offsets after the scan), the in-chunk
+// prefixes of the lengths and the per-group key totals (sized for any
+// grouping of the heads).
 size_t compact_scratch_bytes(int64_t R, int nB) {
   if (R <= 0) return 0;
-  const int64_t G = sort_chunks(R);
+  const int64_t G = max_chunks(R);
   return 2 * align_up((size_t)R * sizeof(int32_t)) + align_up((size_t)(nB + 2) * G * sizeof(int32_t)) +
-         align_up((size_t)G * sizeof(int32_t));
+         align_up((size_t)G * sizeof(int32_t)) + align_up((size_t)63 * (nB + 1) * sizeof(int32_t));
 }
 
 // row_ptr and order from the list lengths, then col_idx by `fill` (built by
-// make_fill from the chunk offsets and in-chunk prefixes); sort_scratch: the
-// part of compact_scratch_bytes after the lengths.
+// make_fill from the chunk offsets, the in-chunk prefixes and the chunks);
+// sort_scratch: the part of compact_scratch_bytes after the lengths.
 template <class MakeFill>
 static hipError_t launch_sort_fill(const int32_t *len, int64_t R, int nB, int32_t *row_ptr,
                                    int32_t *order, int32_t *n_active, void *sort_scratch,
-                                   const MakeFill &make_fill, hipStream_t s) {
-  const int G = sort_chunks(R);
+                                   int64_t group_rows, const MakeFill &make_fill, hipStream_t s) {
+  if (R < 1) return hipErrorInvalidValue;  // G >= 1 below
+  const Chunks ch = make_chunks(R, group_rows);
+  const int ngroups = n_groups(ch);
+  if (ngroups > 63) return hipErrorInvalidValue;
+  // every group's chunks, the last group's only as far as its rows reach
+  const int64_t last = R - (int64_t)(ngroups - 1) * ch.gr;
+  const int G = (ngroups - 1) * ch.cpg + (int)((last + kChunk - 1) / kChunk);
   const int K = nB + 2;
+  const int64_t Gmax = max_chunks(R);
   char *p = static_cast<char *>(sort_scratch);
   int32_t *hist = reinterpret_cast<int32_t *>(p);
-  p += align_up((size_t)K * G * sizeof(int32_t));
+  p += align_up((size_t)K * Gmax * sizeof(int32_t));
   int32_t *csum = reinterpret_cast<int32_t *>(p);
-  p += align_up((size_t)G * sizeof(int32_t));
+  p += align_up((size_t)Gmax * sizeof(int32_t));
   int32_t *rloc = reinterpret_cast<int32_t *>(p);
-  const auto fill = make_fill(csum, rloc);
+  p += align_up((size_t)R * sizeof(int32_t));
+  int32_t *gtot = reinterpret_cast<int32_t *>(p);
+  const auto fill = make_fill(csum, rloc, ch);
   using Fill = std::decay_t<decltype(fill)>;
   const size_t hl = (size_t)K * sizeof(int32_t);
   const size_t pl = (size_t)K * kSortWaves * sizeof(int32_t);
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&place_fill_kernel<Fill>),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(sort_hist_kernel, dim3((unsigned)G), dim3(kScanThreads), hl, s, len, (int)R, nB,
-                     hist, csum, rloc);
-  auto scan = G <= 4 ? sort_scan_kernel<4> : G <= 8 ? sort_scan_kernel<8> : G <= 16 ? sort_scan_kernel<16> : sort_scan_kernel<32>;
-  hipLaunchKernelGGL(scan, dim3(1), dim3(kScanThreads), 0, s, (int)R, nB, G, hist, csum, row_ptr,
-                     n_active);
+  hipLaunchKernelGGL(sort_hist_kernel, dim3((unsigned)G), dim3(kScanThreads), hl, s, len, ch, nB, hist,
+                     csum, rloc);
+  const size_t gl = (size_t)ngroups * (nB + 2) * sizeof(int32_t);
+  if (K <= kScanThreads && G <= 32 && gl <= kScanFastLds) {
+    auto scan = G <= 4 ? sort_scan_fast_kernel<4> : G <= 8 ? sort_scan_fast_kernel<8>
+              : G <= 16 ? sort_scan_fast_kernel<16> : sort_scan_fast_kernel<32>;
+    if ((e = hipFuncSetAttribute(reinterpret_cast<const void *>(scan),
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)gl)) != hipSuccess)
+      return e;
+    hipLaunchKernelGGL(scan, dim3(1), dim3(kScanThreads), gl, s, (int)R, nB, G, ch.cpg, ngroups, hist,
+                       csum, row_ptr, n_active);
+  } else {
+    auto scan = G <= 4 ? sort_scan_kernel<4> : G <= 8 ? sort_scan_kernel<8> : G <= 16 ? sort_scan_kernel<16> : sort_scan_kernel<32>;
+    hipLaunchKernelGGL(scan, dim3(1), dim3(kScanThreads), 0, s, (int)R, nB, G, ch.cpg, ngroups, hist, csum,
+                       gtot, row_ptr, n_active);
+  }
   const int64_t fill_groups = (R + kSortWaves - 1) / kSortWaves;
   hipLaunchKernelGGL(place_fill_kernel<Fill>, dim3((unsigned)(G + fill_groups)), dim3(kScanThreads),
-                     pl, s, len, (int)R, nB, G, hist, csum, rloc, row_ptr, order, fill);
+                     pl, s, len, ch, nB, G, hist, csum, rloc, row_ptr, order, fill);
   return hipGetLastError();
 }
 
-hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_ptr,
-                          int32_t *col_idx, int32_t *order, void *scratch, hipStream_t s) {
+hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int64_t group_rows,
+                          int32_t *row_ptr, int32_t *col_idx, int32_t *order, void *scratch,
+                          hipStream_t s) {
   int32_t *len = static_cast<int32_t *>(scratch);
   void *sort_scratch = static_cast<char *>(scratch) + align_up((size_t)R * sizeof(int32_t));
   const unsigned g = (unsigned)((R + 3) / 4);
@@ -545,9 +730,9 @@ hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_p
 #define CARNATOR_COMPACT(NU)                                                                     \
   do {                                                                                           \
     hipLaunchKernelGGL(count_kernel<NU>, dim3(g), dim3(256), 0, s, mask, R, nB, len);            \
-    return launch_sort_fill(len, R, nB, row_ptr, order, nullptr, sort_scratch,                   \
-                            [&](const int32_t *coff, const int32_t *rloc) {                      \
-                              return FillBytes<NU>{mask, R, nB, coff, rloc, col_idx};            \
+    return launch_sort_fill(len, R, nB, row_ptr, order, nullptr, sort_scratch, group_rows,       \
+                            [&](const int32_t *coff, const int32_t *rloc, Chunks ch) {           \
+                              return FillBytes<NU>{mask, R, nB, coff, rloc, ch, col_idx};        \
                             },                                                                   \
                             s);                                                                  \
   } while (0)
@@ -591,8 +776,8 @@ size_t compact_bits_scratch_bytes(int64_t R, int B, int nB) {
   return compact_scratch_bytes(R, nB) + align_up((size_t)B * ((nB + 63) / 64) * sizeof(uint64_t));
 }
 
-hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const uint8_t *rows,
-                               const uint8_t *cols, bool narrow, int32_t *row_ptr,
+hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, int64_t group_rows,
+                               const uint8_t *rows, const uint8_t *cols, bool narrow, int32_t *row_ptr,
                                int32_t *col_idx, int32_t *order, int32_t *n_active, void *scratch,
                                hipStream_t s) {
   const int64_t R = (int64_t)B * H * nB;
@@ -620,9 +805,9 @@ hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const
     default: return hipErrorInvalidValue;
   }
   return launch_sort_fill(len, R, nB, row_ptr, order, n_active,
-                          static_cast<char *>(scratch) + align_up((size_t)R * sizeof(int32_t)),
-                          [&](const int32_t *coff, const int32_t *rloc) {
-                            return FillBits{bits, (int)R, nB, HnB, rows, colw, narrow, coff, rloc, col_idx};
+                          static_cast<char *>(scratch) + align_up((size_t)R * sizeof(int32_t)), group_rows,
+                          [&](const int32_t *coff, const int32_t *rloc, Chunks ch) {
+                            return FillBits{bits, (int)R, nB, HnB, rows, colw, narrow, coff, rloc, ch, col_idx};
                           },
                           s);
 }

@@ -111,8 +111,16 @@ hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows
 // ---- compaction ------------------------------------------------------------
 // Scratch needed by launch_compact, in bytes (R rows of nB key blocks).
 size_t compact_scratch_bytes(int64_t R, int nB);
-hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int32_t *row_ptr,
-                          int32_t *col_idx, int32_t *order, void *scratch, hipStream_t s);
+// Heads per group of the row order: the most heads whose K and V (bf16,
+// N x d each) fit kOrderGroupBytes, at least one and at least heads / 63;
+// heads when all of them fit.
+constexpr int64_t kOrderGroupBytes = (int64_t)256 << 20;
+int order_group_heads(int heads, int64_t N, int d);
+// group_rows: rows per head group of the order (>= R: the plain
+// longest-first order).
+hipError_t launch_compact(const uint8_t *mask, int64_t R, int nB, int64_t group_rows,
+                          int32_t *row_ptr, int32_t *col_idx, int32_t *order, void *scratch,
+                          hipStream_t s);
 
 // ---- bit-packed masks --------------------------------------------------------
 // R rows of nB keep flags as uint64 [R][ceil(nB / 64)], key block j at bit
@@ -127,8 +135,8 @@ hipError_t launch_fill_ones_bits(uint64_t *bits, int64_t R, int nB, hipStream_t 
 // are kept; order lists the active rows first and *n_active (if not NULL)
 // receives their number.
 size_t compact_bits_scratch_bytes(int64_t R, int B, int nB);
-hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, const uint8_t *rows,
-                               const uint8_t *cols, bool narrow, int32_t *row_ptr,
+hipError_t launch_compact_bits(const uint64_t *bits, int B, int H, int nB, int64_t group_rows,
+                               const uint8_t *rows, const uint8_t *cols, bool narrow, int32_t *row_ptr,
                                int32_t *col_idx, int32_t *order, int32_t *n_active, void *scratch,
                                hipStream_t s);
 

@@ -216,14 +216,30 @@ def test_bit_packed_entry_points_reject(L):
     assert "workspace" in _err(L)
 
 
+def test_order_group_heads(L):
+    g = L.carnator_order_group_heads
+    # heads whose K and V (2 * N * d bf16 values each) fit 256 MiB
+    assert g(ctypes.byref(_shape(1, 12, 32760, 128, 128))) == 12  # 16.8 MB a head: all 12
+    assert g(ctypes.byref(_shape(1, 40, 75600, 128, 128))) == 6  # 38.7 MB: 6
+    assert g(ctypes.byref(_shape(1, 24, 119056, 128, 128))) == 4  # 61.0 MB: 4
+    assert g(ctypes.byref(_shape(2, 24, 119056, 128, 128))) == 4  # groups span the batch
+    assert g(ctypes.byref(_shape(1, 200, 262144, 128, 128))) == 4  # 134 MB: 1, but at most 63 groups
+    assert g(ctypes.byref(_shape(d=96))) == 0
+    assert g(None) == 0
+
+
 def test_bit_packed_workspace_size(L):
     s = _shape(1, 12, 32760, 128, 128)
     R = 12 * 256
-    # the list lengths, the sort's chunk histograms ((nB + 2) keys x 3 chunks
-    # of 1024 rows), chunk offsets and in-chunk prefixes of the lengths, then
-    # the packed dense-column words of each batch entry
-    hist = -(-(258 * 3 * 4) // 256) * 256
-    assert L.carnator_compact_block_mask_bits_workspace_size(ctypes.byref(s)) == 12288 + hist + 256 + 12288 + 256
+    # the list lengths, the sort's chunk histograms ((nB + 2) keys x at most
+    # 3 + 63 chunks of 1024 rows: the rows of up to 63 head groups), chunk
+    # offsets, in-chunk prefixes of the lengths and per-group key totals (63
+    # groups x (nB + 1) keys), then the packed dense-column words of each
+    # batch entry
+    a = lambda n: -(-n // 256) * 256
+    chunks = 3 + 63
+    want = a(R * 4) + a(258 * chunks * 4) + a(chunks * 4) + a(R * 4) + a(63 * 257 * 4) + a(8)
+    assert L.carnator_compact_block_mask_bits_workspace_size(ctypes.byref(s)) == want
     assert L.carnator_compact_block_mask_bits_workspace_size(ctypes.byref(_shape(d=96))) == 0
     assert R * 4 == 12288
 

@@ -85,6 +85,13 @@ def _compare_rows(o_gpu, o_ref, lse_gpu, lse_ref, rows, N, bs):
     assert rel <= REL_L2
 
 
+def _group_heads(m, attn=None):
+    """Heads per group of the row order the library writes for masks shaped
+    like m (and the attention shape attn)."""
+    B, H, nb = m.shape[:3]
+    return P.order_group_heads(B, H, nb, attn)
+
+
 def _sample_rows(wl, merged, rows_flags, heads, n_random=32, seed=0):
     """Every target row of head 0, seeded random rows, and the last block of
     every head."""
@@ -173,10 +180,50 @@ def test_compaction_bit_exact(nb, density, heads):
     m[0, 2, 1] = 1
     dm = torch.as_tensor(m, device=DEV)
     rp, ci, order = P.compact_block_mask(dm)
-    wrp, wci, word = oracle.compact_mask(m)
+    wrp, wci, word = oracle.compact_mask(m, group_heads=_group_heads(m))
     np.testing.assert_array_equal(rp.cpu().numpy(), wrp)
     np.testing.assert_array_equal(ci.cpu().numpy(), wci)
     np.testing.assert_array_equal(order.cpu().numpy(), word)
+
+
+# The row order for the attention shapes whose K and V exceed the 256 MiB
+# Infinity Cache: heads in groups (6 of 40 at 75.6K tokens, 4 of 24 at 119K),
+# each group's rows longest first; from the uint8 mask, from bits and
+# restricted, each equal to the oracle's; the attention's output does not
+# depend on the order.
+# (3, 2048), (6, 2048), (40, 591) and (40, 1024) keep up to 8, 16, 32 and
+# more than 32 steps of 64 positions per wave in the grouping pass.
+@pytest.mark.parametrize("heads,nb,attn,G", [(40, 591, (75600, 128, 128), 6), (24, 931, (119056, 128, 128), 4),
+                                             (5, 300, (38400, 128, 128), 5), (3, 2048, (262144, 128, 128), 2),
+                                             (6, 2048, (262144, 128, 128), 2), (40, 1024, (131072, 128, 128), 4)])
+def test_compaction_grouped_order(heads, nb, attn, G):
+    m = synth.random_mask(1, heads, nb, 0.15, heads)
+    assert P.order_group_heads(1, heads, nb, attn) == G
+    rp, ci, order = P.compact_block_mask(torch.as_tensor(m, device=DEV), attn=attn)
+    wrp, _, word = oracle.compact_mask(m, group_heads=G)
+    np.testing.assert_array_equal(rp.cpu().numpy(), wrp)
+    np.testing.assert_array_equal(order.cpu().numpy(), word)
+    bits = torch.as_tensor(oracle.pack_mask(m).view(np.int64), device=DEV)
+    _, _, order_b = P.compact_block_mask_bits(bits, attn=attn)
+    np.testing.assert_array_equal(order_b.cpu().numpy(), word)
+    rng = np.random.default_rng(heads)
+    act = (rng.random((1, nb)) < 0.3).astype(np.uint8)
+    ctx = np.maximum(act, (rng.random((1, nb)) < 0.5).astype(np.uint8))
+    _, _, order_r, n = P.compact_block_mask_bits_region(bits, act, ctx, attn=attn)
+    _, _, word_r, wn = oracle.compact_restricted(m, act, ctx, group_heads=G)
+    assert int(n.item()) == wn
+    np.testing.assert_array_equal(order_r.cpu().numpy(), word_r)
+
+
+def test_attention_independent_of_row_order():
+    wl, x = _inputs(1, heads=4)
+    mask = P.build_block_mask(x["q_hist"], x["k_hist"], wl.block, wl.tau)
+    rp, ci, order = P.compact_block_mask(mask)
+    o1 = P.block_sparse_attn_lists(x["q"], x["k"], x["v"], (rp, ci, order), wl.block)
+    rev = torch.flip(order, [0]).contiguous()
+    o2 = P.block_sparse_attn_lists(x["q"], x["k"], x["v"], (rp, ci, rev), wl.block)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
 
 
 # ---------------------------------------------------------------- bit-packed masks
@@ -238,7 +285,7 @@ def test_compaction_from_bits_bit_exact(nb, density, heads, widen):
     before = dbits.clone()
     rp, ci, order = P.compact_block_mask_bits(dbits, rows, cols)
     merged = oracle.merge_target_rows(m, rows, cols) if widen else m
-    wrp, wci, word = oracle.compact_mask(merged)
+    wrp, wci, word = oracle.compact_mask(merged, group_heads=_group_heads(merged))
     np.testing.assert_array_equal(rp.cpu().numpy(), wrp)
     np.testing.assert_array_equal(ci.cpu().numpy(), wci)
     np.testing.assert_array_equal(order.cpu().numpy(), word)
@@ -266,7 +313,7 @@ def test_mask_bank_record_and_reuse():
         _assert_masks_equal(torch.as_tensor(got), m, fragile, wl.tau)
         lists = bank.lists(t, c, layer, x["row_flags"])
         merged = oracle.merge_target_rows(got, x["row_flags"].cpu().numpy())
-        for g, w in zip(lists, oracle.compact_mask(merged)):
+        for g, w in zip(lists, oracle.compact_mask(merged, group_heads=_group_heads(merged))):
             np.testing.assert_array_equal(g.cpu().numpy(), w)
         o = P.block_sparse_attn_lists(x["q"], x["k"], x["v"], lists, wl.block)
         o_ref, _ = oracle.block_sparse_attention(oracle.to_f64(x["q"]), oracle.to_f64(x["k"]),

@@ -129,7 +129,7 @@ def test_compaction_region_bit_exact(nb, density, heads, p_act):
     ctx = np.maximum(act, (rng.random((B, nb)) < 0.5).astype(np.uint8))
     bits = torch.as_tensor(oracle.pack_mask(m).view(np.int64), device=DEV)
     rp, ci, order, n = P.compact_block_mask_bits_region(bits, act, ctx)
-    wrp, wci, word, wn = oracle.compact_restricted(m, act, ctx)
+    wrp, wci, word, wn = oracle.compact_restricted(m, act, ctx, group_heads=P.order_group_heads(B, heads, nb))
     assert int(n.item()) == wn
     np.testing.assert_array_equal(rp.cpu().numpy(), wrp)
     np.testing.assert_array_equal(ci[:int(wrp[-1])].cpu().numpy(), wci)

@@ -187,6 +187,35 @@ def test_merge_identities():
 
 # ---------------------------------------------------------------- compaction
 
+def test_compact_grouped_order_by_brute_force():
+    # heads in groups of G: the order is (group, descending length, row), the
+    # definition written out as a sort of tuples; one group (G >= heads) is
+    # the plain longest-first order
+    rng = np.random.default_rng(11)
+    m = (rng.random((2, 5, 7, 7)) < 0.4).astype(np.uint8)
+    m[1, 2, 4] = 0
+    nb = 7
+    flat = m.reshape(-1, nb)
+    lens = flat.sum(axis=1)
+    R = flat.shape[0]
+    for G in (1, 2, 3, 4, 10, 11):
+        _, _, order = oracle.compact_mask(m, group_heads=G)
+        want = sorted(range(R), key=lambda r: (r // (G * nb), -int(lens[r]), r))
+        assert order.tolist() == want, G
+    np.testing.assert_array_equal(oracle.compact_mask(m, group_heads=10)[2], oracle.compact_mask(m)[2])
+    # restricted lists: the active rows grouped the same way, the inactive
+    # rows after them in row order
+    act = (rng.random((2, nb)) < 0.6).astype(np.uint8)
+    ctx = np.ones((2, nb), np.uint8)
+    for G in (2, 3):
+        rp, _, order, n_act = oracle.compact_restricted(m, act, ctx, group_heads=G)
+        rl = np.diff(rp)
+        active = np.broadcast_to(act[:, None, :] != 0, (2, 5, nb)).reshape(-1)
+        want = sorted([r for r in range(R) if active[r]], key=lambda r: (r // (G * nb), -int(rl[r]), r))
+        want += [r for r in range(R) if not active[r]]
+        assert order.tolist() == want and n_act == int(active.sum())
+
+
 def test_compact_roundtrip_and_order():
     rng = np.random.default_rng(5)
     m = (rng.random((1, 4, 9, 9)) < 0.35).astype(np.uint8)
