@@ -49,21 +49,55 @@ struct Chunks {
   }
 };
 
-// One thread per mask byte.
+// Sixteen bytes of the flat mask per thread (one 16-byte load and store when
+// the mask is 16-byte aligned); a thread's bytes may run over row ends, so
+// it finds (b, h, i, j) of its first byte once and steps from there.
+// B*H*nB*nB < 2^31 (the shape check), so 32-bit indices.
 __global__ void __launch_bounds__(256) merge_kernel(uint8_t *__restrict__ mask, int H, int nB,
-                                                    int64_t total,
+                                                    int total, bool vec,
                                                     const uint8_t *__restrict__ rows,
                                                     const uint8_t *__restrict__ cols) {
-  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (x >= total) return;
-  const int64_t nb2 = (int64_t)nB * nB;
-  const int64_t bh = x / nb2;
-  const int b = (int)(bh / H);
-  const int rem = (int)(x - bh * nb2);
-  const int i = rem / nB, j = rem - i * nB;
-  const bool keep = mask[x] != 0 || rows[(int64_t)b * nB + i] != 0 ||
-                    (cols != nullptr && cols[(int64_t)b * nB + j] != 0);
-  mask[x] = keep ? 1 : 0;
+  const int64_t x64 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 16;
+  if (x64 >= total) return;
+  const int x0 = (int)x64;
+  const int n = min(16, total - x0);
+  const int gr = x0 / nB;  // row of the flat mask: (b * H + h) * nB + i
+  int j = x0 - gr * nB;
+  const int bh = gr / nB;
+  int i = gr - bh * nB;
+  int b = bh / H;
+  int h = bh - b * H;
+  union {
+    uint4 q;
+    uint8_t c[16];
+  } v;
+  if (vec && n == 16) {
+    v.q = *reinterpret_cast<const uint4 *>(mask + x0);
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v.c[k] = k < n ? mask[x0 + k] : 0;
+  }
+  bool rf = rows[b * nB + i] != 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const bool cf = cols != nullptr && k < n && cols[b * nB + j] != 0;
+    v.c[k] = (v.c[k] != 0 || rf || cf) ? 1 : 0;
+    if (++j == nB) {  // the next byte starts a row
+      j = 0;
+      if (++i == nB) {
+        i = 0;
+        if (++h == H) h = 0, ++b;
+      }
+      rf = k + 1 < n && rows[b * nB + i] != 0;
+    }
+  }
+  if (vec && n == 16) {
+    *reinterpret_cast<uint4 *>(mask + x0) = v.q;
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      if (k < n) mask[x0 + k] = v.c[k];
+  }
 }
 
 // A row's mask bytes, lane l holding columns l, l + 64, ... (NC of them, at
@@ -626,9 +660,11 @@ __global__ void __launch_bounds__(kScanThreads) place_fill_kernel(const int32_t 
 
 hipError_t launch_merge(uint8_t *mask, int B, int H, int nB, const uint8_t *rows,
                         const uint8_t *cols, hipStream_t s) {
-  const int64_t total = (int64_t)B * H * nB * nB;
-  hipLaunchKernelGGL(merge_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, mask, H,
-                     nB, total, rows, cols);
+  const int64_t total = (int64_t)B * H * nB * nB;  // < 2^31 (the shape check)
+  const bool vec = reinterpret_cast<uintptr_t>(mask) % 16 == 0;
+  const int64_t threads = (total + 15) / 16;
+  hipLaunchKernelGGL(merge_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, mask, H,
+                     nB, (int)total, vec, rows, cols);
   return hipGetLastError();
 }
 

@@ -164,6 +164,27 @@ def test_merge_bit_exact(wid):
     np.testing.assert_array_equal(got, oracle.merge_target_rows(m, rows, cols))
 
 
+# Rows shorter than, equal to and just over the 16 bytes a thread widens (a
+# thread's bytes then span several rows, heads and batch entries), with and
+# without dense columns, from 16-byte aligned and unaligned mask addresses.
+@pytest.mark.parametrize("nb", [1, 3, 15, 16, 17, 33, 130])
+@pytest.mark.parametrize("offset", [0, 1, 7])
+def test_merge_short_rows_and_unaligned(nb, offset):
+    rng = np.random.default_rng(nb * 10 + offset)
+    B, H = 2, 3
+    m = (rng.random((B, H, nb, nb)) < 0.3).astype(np.uint8) * rng.integers(1, 255, (B, H, nb, nb), dtype=np.uint8)
+    rows = (rng.random((B, nb)) < 0.2).astype(np.uint8)
+    cols = (rng.random((B, nb)) < 0.2).astype(np.uint8)
+    for c in (cols, None):
+        buf = torch.zeros(m.size + offset + 16, dtype=torch.uint8, device=DEV)
+        dm = buf[offset:offset + m.size].view(m.shape)
+        dm.copy_(torch.as_tensor(m))
+        P.merge_target_rows(dm, rows, c)
+        np.testing.assert_array_equal(dm.cpu().numpy(), oracle.merge_target_rows(m, rows, c))
+        # the bytes around the mask are untouched
+        assert int(buf[:offset].sum()) == 0 and int(buf[offset + m.size:].sum()) == 0
+
+
 # R = heads * nb rows in chunks of 1024: one chunk up to (931, 1); 3, 5, 10,
 # 14 and 22 chunks (the last partial) keep a key's chunk counts in registers
 # in the scan; (2048, 17) has 34 chunks and takes the two-pass scan.  Rows of
