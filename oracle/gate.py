@@ -29,8 +29,9 @@ Readings (the paper is silent on these points):
 3. The Clopper-Pearson upper bound at u = n is 1.
 
 Pins: ``ciede2000`` is pinned in its lightness and chroma terms by closed
-forms; its hue weighting (T, delta-theta, R_T, S_H) only by symmetry and
-hue-wrap continuity, so d_color is parity unpinned in those terms.
+forms, and as a whole (the hue weighting T, delta-theta, R_T, S_H included)
+by LittleCMS's independent cmsCIE2000DeltaE on random, close,
+near-achromatic and hue-wrap pairs (within 1e-9).
 """
 import math
 

@@ -113,3 +113,53 @@ def test_discrepancies_and_gate():
     d = [[0, 0, 0, 8.0], [2.0, 0, 0, 0], [0.5, 1.0, 0.4, 3.0], [0, 0, 0, 0]]
     assert oracle.first_compatible(d, tau) == 2
     assert oracle.first_compatible(d[:2], tau) == -1
+
+
+# An independent implementation of CIEDE2000: LittleCMS's cmsCIE2000DeltaE
+# (its documented C API, weights kL, kC, kH), called through ctypes on the
+# system's liblcms2.  It pins the hue weighting (T, delta-theta, R_T, S_H)
+# that no closed form above reaches: random pairs over the whole gamut, close
+# pairs, near-achromatic pairs, and a grid of hue pairs around the wrap at 0
+# and 360 degrees, R_T's peak at 275 degrees and opposite hues, with zero and
+# unequal chromas.
+def _lcms_de2000():
+    import ctypes
+    import ctypes.util
+    name = ctypes.util.find_library("lcms2") or "liblcms2.so.2"
+    try:
+        lib = ctypes.CDLL(name)
+    except OSError:
+        return None
+
+    class Lab(ctypes.Structure):
+        _fields_ = [("L", ctypes.c_double), ("a", ctypes.c_double), ("b", ctypes.c_double)]
+
+    f = lib.cmsCIE2000DeltaE
+    f.restype = ctypes.c_double
+    f.argtypes = [ctypes.POINTER(Lab), ctypes.POINTER(Lab), ctypes.c_double, ctypes.c_double, ctypes.c_double]
+    return lambda p, q: f(ctypes.byref(Lab(*map(float, p))), ctypes.byref(Lab(*map(float, q))), 1.0, 1.0, 1.0)
+
+
+def test_ciede2000_against_littlecms():
+    de = _lcms_de2000()
+    if de is None:
+        pytest.skip("liblcms2 is not installed")
+    rng = np.random.default_rng(3)
+    pairs = []
+    for it in range(3000):
+        p = rng.uniform([0, -128, -128], [100, 128, 128], size=(2, 3))
+        if it % 3 == 1:
+            p[1] = p[0] + rng.normal(0, 3, 3)  # close pairs
+        if it % 3 == 2:
+            p[:, 1:] *= rng.uniform(0, 0.05)  # near-achromatic
+        pairs.append((p[0], p[1]))
+    for L1, L2 in [(50, 50), (50, 60), (20, 90)]:
+        for h1 in [0, 10, 90, 170, 180, 190, 270, 275, 300, 350, 359.9]:
+            for h2 in [0, 5, 95, 185, 200, 275, 355, 359]:
+                for C1, C2 in [(30, 30), (0, 40), (40, 0), (0, 0), (5, 80)]:
+                    r1, r2 = math.radians(h1), math.radians(h2)
+                    pairs.append((np.array([L1, C1 * math.cos(r1), C1 * math.sin(r1)]),
+                                  np.array([L2, C2 * math.cos(r2), C2 * math.sin(r2)])))
+    got = oracle.ciede2000(np.stack([p for p, _ in pairs]), np.stack([q for _, q in pairs]))
+    want = np.array([de(p, q) for p, q in pairs])
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-9)
