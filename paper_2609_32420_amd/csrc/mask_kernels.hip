@@ -99,6 +99,95 @@ __device__ inline double key_value(uint64_t k) {
   return __longlong_as_double((long long)b);
 }
 
+// Bisection state of one row (the same in every lane): mass(key >= lo) >=
+// tau Z > mass(key >= hi), cnt_* the numbers of keys >= lo and >= hi.
+struct Bisect {
+  uint64_t lo, hi;
+  int cnt_lo, cnt_hi;
+  double m_hi;  // mass of the keys >= hi
+  bool trie;
+  int it;
+};
+
+// Bisection steps over EE positions per lane until at most `until` keys lie
+// in [lo, hi).  The keys counted are those of the positions plus c_off, the
+// mass their weights plus m_off (the keys above the positions' range).
+// Split at the midpoint of the values while that separates keys; once it
+// does not (a run of equal logits), split at the highest bit in which the
+// interval's smallest and largest keys differ, which leaves keys on both
+// sides and resolves equal logits by their index bits.
+template <int EE>
+__device__ inline void bisect_steps(const uint64_t (&key)[EE], const double (&pl)[EE], int c_off,
+                                    double m_off, double tauZ, int until, Bisect &b) {
+  for (; b.it < 192 && b.cnt_lo - b.cnt_hi > until; ++b.it) {
+    uint64_t K = 0;
+    if (!b.trie) {
+      const double lv = key_value(b.lo), hv = key_value(b.hi - 1);
+      K = sel_key(uniform(lv + 0.5 * (hv - lv)), 2047);
+      b.trie = !(K > b.lo && K < b.hi);
+    }
+    if (b.trie) {
+      uint64_t a = ~0ull, z = 0ull;
+#pragma unroll
+      for (int u = 0; u < EE; ++u) {
+        const bool in = key[u] >= b.lo && key[u] < b.hi;
+        a = in && key[u] < a ? key[u] : a;
+        z = in && key[u] > z ? key[u] : z;
+      }
+      a = wave_min_u64(a);
+      z = wave_max_u64(z);
+      // a < z: the interval holds at least two (distinct) keys
+      K = z & ~((1ull << (63 - __clzll((long long)(a ^ z)))) - 1ull);
+    }
+    double m = 0.0;
+    int c = c_off;
+#pragma unroll
+    for (int u = 0; u < EE; ++u) {
+      const bool ge = key[u] >= K;
+      m += ge ? pl[u] : 0.0;
+      c += __popcll(__ballot(ge));
+    }
+    m = m_off + wave_sum(m);
+    const int before = b.cnt_lo - b.cnt_hi;
+    if (m >= tauZ) {
+      b.lo = K;
+      b.cnt_lo = c;
+    } else {
+      b.hi = K;
+      b.cnt_hi = c;
+      b.m_hi = m;
+    }
+    if (b.cnt_lo - b.cnt_hi == before) b.trie = true;
+  }
+}
+
+// The k-th largest key once the bisection has ended: the one key in [lo, hi)
+// (k = cnt_lo), or, if the step cap was hit, the largest key in [lo, hi) and
+// the number of keys at or above it.
+template <int EE>
+__device__ inline uint64_t bisect_result(const uint64_t (&key)[EE], int c_off, const Bisect &b,
+                                         int &k) {
+  uint64_t kstar = 0ull;
+  if (b.cnt_lo - b.cnt_hi == 1) {
+#pragma unroll
+    for (int u = 0; u < EE; ++u) {
+      const unsigned long long hit = __ballot(key[u] >= b.lo && key[u] < b.hi);
+      if (hit) kstar = read_lane(key[u], __ffsll((long long)hit) - 1);
+    }
+    k = b.cnt_lo;
+  } else {
+    uint64_t kl = 0ull;
+#pragma unroll
+    for (int u = 0; u < EE; ++u)
+      if (key[u] >= b.lo && key[u] < b.hi && key[u] > kl) kl = key[u];
+    kstar = wave_max_u64(kl);
+    k = c_off;
+#pragma unroll
+    for (int u = 0; u < EE; ++u) k += __popcll(__ballot(key[u] >= kstar));
+  }
+  return kstar;
+}
+
 // One workgroup of W waves per (bh, R consecutive query blocks), W = R or
 // R / 2 (then each wave selects two rows).
 //
@@ -122,7 +211,8 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
                                                         uint8_t *__restrict__ mask,
                                                         uint64_t *__restrict__ bits, int BH) {
   // LDS: [R][nB] logits, then the R pooled query rows, QS doubles apart (a
-  // 16-byte pad spreads the 16 rows read by one MFMA step over the banks)
+  // 16-byte pad spreads the 16 rows read by one MFMA step over the banks),
+  // at least W * 128 doubles
   constexpr int QS = D + 2;
   extern __shared__ double sc[];
   // Workgroups are dealt to the 8 XCDs in turn.  Logical workgroup
@@ -141,6 +231,9 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
   const double *kb = kbar + (int64_t)bh * nB * D;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  // phase 2's candidate buffers (64 keys and weights per wave) reuse the
+  // pooled-row area, which phase 1's last barrier frees
+  uint64_t *cbuf = reinterpret_cast<uint64_t *>(sc + R * nB);
 
   if constexpr (MASS) {
     const double *src = qbar + ((int64_t)bh * nB + r0) * nB;
@@ -242,83 +335,65 @@ __global__ void __launch_bounds__(64 * W) select_kernel(const double *__restrict
     }
     const double tauZ = tau * wave_sum(lsum);
 
-    // whether the keys >= K reach tau, and their count (the same in every lane)
-    auto mass_ge = [&](uint64_t K, int &cnt) __attribute__((always_inline)) {
+    // every key lies in [smallest key of value smin, largest key of smax]
+    Bisect bs{sel_key(smin, 2047), sel_key(smax, 0) + 1, 0, 0, 0.0, false, 0};
+    bool reach;
+    {
       double m = 0.0;
       int c = 0;
 #pragma unroll
       for (int u = 0; u < E; ++u) {
-        const bool ge = key[u] >= K;
+        const bool ge = key[u] >= bs.lo;
         m += ge ? pl[u] : 0.0;
         c += __popcll(__ballot(ge));
       }
-      cnt = c;
-      return wave_sum(m) >= tauZ;
-    };
-    // every key lies in [smallest key of value smin, largest key of smax]
-    uint64_t lo = sel_key(smin, 2047), hi = sel_key(smax, 0) + 1;
-    int cnt_lo, cnt_hi = 0;
+      bs.cnt_lo = c;
+      reach = wave_sum(m) >= tauZ;
+    }
     int k;
     double cut;
-    if (!mass_ge(lo, cnt_lo)) {
-      k = cnt_lo;  // the whole row falls short of tau: keep every block
+    if (!reach) {
+      k = bs.cnt_lo;  // the whole row falls short of tau: keep every block
       cut = smin;
     } else {
-      // Split at the midpoint of the values while that separates keys; once
-      // it does not (a run of equal logits), split at the highest bit in
-      // which the interval's smallest and largest keys differ, which leaves
-      // keys on both sides and resolves equal logits by their index bits.
-      bool trie = false;
-      for (int it = 0; it < 192 && cnt_lo - cnt_hi > 1; ++it) {
-        uint64_t K = 0;
-        if (!trie) {
-          const double lv = key_value(lo), hv = key_value(hi - 1);
-          K = sel_key(uniform(lv + 0.5 * (hv - lv)), 2047);
-          trie = !(K > lo && K < hi);
-        }
-        if (trie) {
-          uint64_t a = ~0ull, b = 0ull;
+      uint64_t kstar;
+      if constexpr (E == 1) {
+        bisect_steps<1>(key, pl, 0, 0.0, tauZ, 1, bs);
+        kstar = bisect_result<1>(key, 0, bs, k);
+      } else {
+        // all positions until at most 64 keys are left in [lo, hi); those
+        // keys and weights then go one per lane (through this wave's LDS
+        // area), and the remaining steps touch one position per lane
+        bisect_steps<E>(key, pl, 0, 0.0, tauZ, 64, bs);
+        if (bs.cnt_lo - bs.cnt_hi > 64) {
+          kstar = bisect_result<E>(key, 0, bs, k);  // the step cap was hit
+        } else {
+          uint64_t *ck = cbuf + wave * 128;
+          double *cw = reinterpret_cast<double *>(ck + 64);
+          int base = 0;
 #pragma unroll
           for (int u = 0; u < E; ++u) {
-            const bool in = key[u] >= lo && key[u] < hi;
-            a = in && key[u] < a ? key[u] : a;
-            b = in && key[u] > b ? key[u] : b;
+            const bool in = key[u] >= bs.lo && key[u] < bs.hi;
+            const unsigned long long hit = __ballot(in);
+            if (in) {
+              const int x = base + __popcll(hit & ((1ull << lane) - 1ull));
+              ck[x] = key[u];
+              cw[x] = pl[u];
+            }
+            base += __popcll(hit);
           }
-          a = wave_min_u64(a);
-          b = wave_max_u64(b);
-          // a < b: the interval holds at least two (distinct) keys
-          K = b & ~((1ull << (63 - __clzll((long long)(a ^ b)))) - 1ull);
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+          // empty lanes hold key 0, below every valid key (> 2047)
+          uint64_t k1[1] = {lane < base ? ck[lane] : 0ull};
+          double p1[1] = {lane < base ? cw[lane] : 0.0};
+          const int c_off = bs.cnt_hi;
+          const double m_off = bs.m_hi;
+          bisect_steps<1>(k1, p1, c_off, m_off, tauZ, 1, bs);
+          kstar = bisect_result<1>(k1, c_off, bs, k);
+          __builtin_amdgcn_wave_barrier();  // the next row's compaction writes the same area
         }
-        const int before = cnt_lo - cnt_hi;
-        int c;
-        if (mass_ge(K, c)) {
-          lo = K;
-          cnt_lo = c;
-        } else {
-          hi = K;
-          cnt_hi = c;
-        }
-        if (cnt_lo - cnt_hi == before) trie = true;
-      }
-      uint64_t kstar = 0ull;
-      if (cnt_lo - cnt_hi == 1) {
-        // the one key in [lo, hi), read from the lane that holds it
-#pragma unroll
-        for (int u = 0; u < E; ++u) {
-          const unsigned long long hit = __ballot(key[u] >= lo && key[u] < hi);
-          if (hit) kstar = read_lane(key[u], __ffsll((long long)hit) - 1);
-        }
-        k = cnt_lo;
-      } else {
-        // the step cap was hit: the largest key in [lo, hi)
-        uint64_t kl = 0ull;
-#pragma unroll
-        for (int u = 0; u < E; ++u)
-          if (key[u] >= lo && key[u] < hi && key[u] > kl) kl = key[u];
-        kstar = wave_max_u64(kl);
-        k = 0;
-#pragma unroll
-        for (int u = 0; u < E; ++u) k += __popcll(__ballot(key[u] >= kstar));
       }
       cut = row[sel_index(kstar)];
     }
@@ -380,7 +455,8 @@ static hipError_t launch_select_dr(const double *qbar, const double *kbar, int B
                                    hipStream_t s) {
   const int G = (nB + R - 1) / R * BH;
   dim3 grid((G + 7) / 8 * 8);
-  const size_t lds = (size_t)R * (nB + D + 2) * sizeof(double);
+  // the logits, then the pooled rows or phase 2's candidate buffers
+  const size_t lds = ((size_t)R * nB + (size_t)max(R * (D + 2), W * 128)) * sizeof(double);
   const int need = (nB + 63) / 64;  // positions per lane
 #define CARNATOR_SEL(EE)                                                                          \
   do {                                                                                            \
@@ -416,9 +492,10 @@ static hipError_t launch_select_dr(const double *qbar, const double *kbar, int B
   return hipGetLastError();
 }
 
-// R query blocks per workgroup: their logits and pooled rows take
-// 8 R (nB + d + 2) bytes of LDS, within 160 KiB for R = 16 up to nB = 1024
-// and for R = 8 up to nB = 2048.  R = 16 fills the 16-row fp64 MFMA tiles
+// R query blocks per workgroup: their logits and pooled rows (or the
+// selection's candidate buffers, 1 KiB per wave) take 8 (R nB + max(R (d + 2),
+// 128 W)) bytes of LDS, within 160 KiB for R = 16 up to nB = 1024 and for
+// R = 8 up to nB = 2048.  R = 16 fills the 16-row fp64 MFMA tiles
 // and halves the kbar re-reads.  W = 16 waves (one row each) while a lane's
 // share of a row (E <= 8 positions) fits the 128 registers of a 1024-thread
 // workgroup, else W = 8 (two rows each when R = 16).
