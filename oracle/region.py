@@ -32,8 +32,9 @@ Readings (the paper is silent on these points):
    and as context.
 6. Rows of inactive query blocks are not computed at all: the restricted
    lists order the active rows first (longest first, lower row on equal
-   length), then the inactive rows in row order, and report how many rows are
-   active; the attention walks only those.
+   length; per group of heads when a group size is given, as in
+   ``compact_mask``), then the inactive rows in row order, and report how many
+   rows are active; the attention walks only those.
 """
 import numpy as np
 

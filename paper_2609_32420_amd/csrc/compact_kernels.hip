@@ -4,9 +4,11 @@
 // Widening (Sec. 3.3, joint reuse in the middle layers): a target-specific
 // query block evaluates every key block, and dense text key blocks are kept
 // in every row.  Compaction produces the list the sparse executor walks:
-// row_ptr / col_idx (ascending key blocks per row) and an order of rows by
-// descending list length (lower row first on equal length), so the longest
-// rows start first.
+// row_ptr / col_idx (ascending key blocks per row) and an order of rows:
+// the heads in consecutive groups whose K and V fit the Infinity Cache
+// (order_group_heads), group after group, and inside a group the rows by
+// descending list length (lower row first on equal length), so a group's
+// longest rows start first.
 //
 // Bit-packed masks (the stored form of the reused connectivity, one bit per
 // block pair): uint64 [rows][nw], nw = ceil(nB / 64), key block j of a row
