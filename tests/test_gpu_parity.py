@@ -212,14 +212,20 @@ def test_compaction_bit_exact(nb, density, heads):
 # each group's rows longest first; from the uint8 mask, from bits and
 # restricted, each equal to the oracle's; the attention's output does not
 # depend on the order.
-# (3, 2048), (6, 2048), (40, 591) and (40, 1024) keep up to 8, 16, 32 and
-# more than 32 steps of 64 positions per wave in the grouping pass.
-@pytest.mark.parametrize("heads,nb,attn,G", [(40, 591, (75600, 128, 128), 6), (24, 931, (119056, 128, 128), 4),
-                                             (5, 300, (38400, 128, 128), 5), (3, 2048, (262144, 128, 128), 2),
-                                             (6, 2048, (262144, 128, 128), 2), (40, 1024, (131072, 128, 128), 4)])
-def test_compaction_grouped_order(heads, nb, attn, G):
-    m = synth.random_mask(1, heads, nb, 0.15, heads)
-    assert P.order_group_heads(1, heads, nb, attn) == G
+# nB = 591 and 931 take the single-pass scan (a thread per key, group totals
+# in LDS), nB = 1024 and 2048 the scan through memory (more keys than
+# threads; 40 chunks at (40, 1024)); (2, 20, 591) has groups of 6 heads
+# across the two batch entries; (1, 5, 300) is one group.
+@pytest.mark.parametrize("batch,heads,nb,attn,G", [(1, 40, 591, (75600, 128, 128), 6),
+                                                   (1, 24, 931, (119056, 128, 128), 4),
+                                                   (2, 20, 591, (75600, 128, 128), 6),
+                                                   (1, 5, 300, (38400, 128, 128), 5),
+                                                   (1, 3, 2048, (262144, 128, 128), 2),
+                                                   (1, 6, 2048, (262144, 128, 128), 2),
+                                                   (1, 40, 1024, (131072, 128, 128), 4)])
+def test_compaction_grouped_order(batch, heads, nb, attn, G):
+    m = synth.random_mask(batch, heads, nb, 0.15, heads)
+    assert P.order_group_heads(batch, heads, nb, attn) == G
     rp, ci, order = P.compact_block_mask(torch.as_tensor(m, device=DEV), attn=attn)
     wrp, _, word = oracle.compact_mask(m, group_heads=G)
     np.testing.assert_array_equal(rp.cpu().numpy(), wrp)
@@ -228,8 +234,8 @@ def test_compaction_grouped_order(heads, nb, attn, G):
     _, _, order_b = P.compact_block_mask_bits(bits, attn=attn)
     np.testing.assert_array_equal(order_b.cpu().numpy(), word)
     rng = np.random.default_rng(heads)
-    act = (rng.random((1, nb)) < 0.3).astype(np.uint8)
-    ctx = np.maximum(act, (rng.random((1, nb)) < 0.5).astype(np.uint8))
+    act = (rng.random((batch, nb)) < 0.3).astype(np.uint8)
+    ctx = np.maximum(act, (rng.random((batch, nb)) < 0.5).astype(np.uint8))
     _, _, order_r, n = P.compact_block_mask_bits_region(bits, act, ctx, attn=attn)
     _, _, word_r, wn = oracle.compact_restricted(m, act, ctx, group_heads=G)
     assert int(n.item()) == wn
