@@ -16,7 +16,8 @@
 // that a query's scores sit in one lane pair.  After key block j each query
 // records (m_j, s_j): its running maximum (log2 units) and the block's
 // sum of 2^(x - m_j); at the end its log2-sum-exp L.  Pass 2
-// (mass_reduce_kernel) forms M_ij = sum_a s_j 2^(m_j - L) / n_i in fp64.
+// (mass_reduce_kernel) forms M_ij = sum_a s_j 2^(m_j - L) / n_i (the powers in
+// fp32, the sum in fp64).
 // The records are block-major ([bh][j][a]) so a wave's 32 queries write 256
 // contiguous bytes.
 #include "internal.h"
@@ -226,27 +227,46 @@ mass_pass_kernel(View q, View k, int H, int N, int nB, int bh0, float c2,
   if (hh == 0 && qv1) lse2[(int64_t)bc * N + a1] = s1.m_run + log2f(s1.l_run);
 }
 
-// One wave per (bh, i, j): M_ij = sum over the valid queries a of block i of
-// s 2^(m - L_a), divided by their number, in fp64.
+// One wave per (bh, i): lane l holds queries a0 + l and a0 + 64 + l of block
+// i (the valid ones among them) and their L; the wave walks the key blocks
+// j, eight at a time with all their record loads in flight, and forms
+// M_ij = sum_a s 2^(m - L_a) / n_i with one wave sum per j.  2^(m - L) is
+// taken in fp32 (m <= L, both fp32 log2 values; relative error ~1e-6) and
+// the terms are summed in fp64.
+constexpr int kReduceUnroll = 8;
 __global__ void __launch_bounds__(256) mass_reduce_kernel(const float2 *__restrict__ rec,
                                                           const float *__restrict__ lse2, int N,
-                                                          int nB, int bs, int64_t total,
+                                                          int nB, int bs, int rows,
                                                           double *__restrict__ mass) {
-  const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int w = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (w >= total) return;
-  const int j = (int)(w % nB);
-  const int64_t bhi = w / nB;
-  const int i = (int)(bhi % nB);
-  const int64_t bh = bhi / nB;
+  if (w >= rows) return;  // the whole wave
+  const int i = w % nB, bh = w / nB;
   const int a0 = i * bs, a1 = min(a0 + bs, N);
-  double acc = 0.0;
-  for (int a = a0 + lane; a < a1; a += 64) {
-    const float2 r = rec[(bh * nB + j) * N + a];
-    acc += (double)r.y * exp2((double)r.x - (double)lse2[bh * N + a]);
+  const int qa = a0 + lane, qb = a0 + 64 + lane;
+  const bool va = qa < a1, vb = qb < a1;
+  const int ca = min(qa, N - 1), cb = min(qb, N - 1);  // clamped: loads stay in the head
+  const float *lh = lse2 + (int64_t)bh * N;
+  const float La = lh[ca], Lb = lh[cb];
+  const float2 *rh = rec + (int64_t)bh * nB * N;
+  const double inv = 1.0 / (double)(a1 - a0);
+  double *out = mass + (int64_t)w * nB;
+  for (int j0 = 0; j0 < nB; j0 += kReduceUnroll) {
+    float2 ra[kReduceUnroll], rb[kReduceUnroll];
+#pragma unroll
+    for (int u = 0; u < kReduceUnroll; ++u) {
+      const float2 *rj = rh + (int64_t)min(j0 + u, nB - 1) * N;
+      ra[u] = rj[ca];
+      rb[u] = rj[cb];
+    }
+#pragma unroll
+    for (int u = 0; u < kReduceUnroll; ++u) {
+      double t = va ? (double)(ra[u].y * __builtin_amdgcn_exp2f(ra[u].x - La)) : 0.0;
+      t += vb ? (double)(rb[u].y * __builtin_amdgcn_exp2f(rb[u].x - Lb)) : 0.0;
+      t = wave_sum(t);
+      if (lane == 0 && j0 + u < nB) out[j0 + u] = t * inv;
+    }
   }
-  acc = wave_sum(acc);
-  if (lane == 0) mass[w] = acc / (double)(a1 - a0);
 }
 
 }  // namespace
@@ -300,9 +320,9 @@ hipError_t launch_mass(View q, View k, int B, int H, int N, int d, int bs, float
     else if (d == 64 && bs == 128) CARNATOR_MASS(64, 128);
     else CARNATOR_MASS(64, 64);
 #undef CARNATOR_MASS
-    const int64_t total = (int64_t)nh * nB * nB;
-    hipLaunchKernelGGL(mass_reduce_kernel, dim3((unsigned)((total + 3) / 4)), dim3(256), 0, s, rec,
-                       lse2, N, nB, bs, total, mass + (int64_t)bh0 * nB * nB);
+    const int rows = nh * nB;
+    hipLaunchKernelGGL(mass_reduce_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, rec,
+                       lse2, N, nB, bs, rows, mass + (int64_t)bh0 * nB * nB);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;
