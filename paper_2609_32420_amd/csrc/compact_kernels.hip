@@ -585,11 +585,15 @@ __global__ void __launch_bounds__(kScanThreads) sort_scan_fast_kernel(int R, int
   __syncthreads();
   if (on) {
     int j = 0, g = 0;
+    int off = gt[slot0];  // the key's start in group g
 #pragma unroll
     for (int u = 0; u < REGS; ++u) {
       if (u < G) {
-        if (j == cpg) j = 0, ++g;
-        hist[(int64_t)u * K + t] = pre[u] + gt[slot0 + g * gstride];
+        if (j == cpg) {
+          j = 0, ++g;
+          off = gt[slot0 + g * gstride];
+        }
+        hist[(int64_t)u * K + t] = pre[u] + off;
         ++j;
       }
     }
