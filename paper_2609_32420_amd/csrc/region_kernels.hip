@@ -47,7 +47,23 @@ __global__ void __launch_bounds__(kRegionThreads) region_kernel(
   uint8_t *ev = fr, *rowd = fr + staged;
   const int64_t base = (int64_t)frame * H * W;
   const int t = threadIdx.x;
-  for (int p = t; p < staged; p += kRegionThreads) ev[p] = evidence[base + (int64_t)ya * W + p] != 0;
+  {
+    // four loads in flight per thread before any is stored
+    const uint8_t *src = evidence + base + (int64_t)ya * W;
+    for (int p0 = 0; p0 < staged; p0 += 4 * kRegionThreads) {
+      uint8_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int p = p0 + u * kRegionThreads + t;
+        v[u] = src[min(p, staged - 1)];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int p = p0 + u * kRegionThreads + t;
+        if (p < staged) ev[p] = v[u] != 0;
+      }
+    }
+  }
   __syncthreads();
   for (int p = t; p < staged; p += kRegionThreads) {
     const int ly = p / W, x = p - ly * W;
@@ -104,6 +120,10 @@ __global__ void __launch_bounds__(256) weight_kernel(const uint8_t *__restrict__
   const int64_t xl = (x0 + 255 < total ? x0 + 255 : total - 1);
   const int64_t b0 = x0 / per_batch, b1 = xl / per_batch;
   const int64_t myb = (x < total ? x : xl) / per_batch;
+  // this thread's token first: its loads are in flight during the walk
+  const int64_t xc = x < total ? x : total - 1;
+  const uint8_t code = region[xc];
+  const uint8_t dd = dist[xc];
   int m = 1;
   for (int64_t bb = b0; bb <= b1; ++bb) {
     int v = 0;
@@ -116,12 +136,11 @@ __global__ void __launch_bounds__(256) weight_kernel(const uint8_t *__restrict__
     if (bb == myb) m = max(m, v);
   }
   if (x >= total) return;
-  const uint8_t code = region[x];
   float w = 0.f;
   if (code == 3) {
     w = 1.f;
   } else if (code == 2) {
-    const float s = (float)dist[x] / (float)m;
+    const float s = (float)dd / (float)m;
     w = 1.f - s * s * (3.f - 2.f * s);
   }
   weight[x] = w;
