@@ -48,8 +48,10 @@
  *   (the default stream).
  * - Ownership: the caller owns every buffer, the workspace and the stream.
  *   The library allocates no device memory, keeps no pointer after it returns
- *   and holds no global mutable state apart from a thread-local error string.
- *   Calls that run concurrently need separate workspaces.
+ *   and holds no global mutable state apart from a thread-local error string
+ *   and, for carnator_signature_sim_noalloc only, a static device scratch
+ *   array and its address on each device.  Calls that run concurrently need
+ *   separate workspaces.
  * - Errors: each call returns a carnator_status.  On a non-OK status nothing
  *   has been enqueued and no output has been written.  All argument checks
  *   happen before the first HIP call.  A failed launch returns
@@ -60,7 +62,8 @@
  *   arbitrary element strides for B, H and N (stride_n a multiple of 8,
  *   data 16-byte aligned).  The attention calls also need stride_n of Q, K
  *   and V at most 2^24 elements (a tile's rows are addressed by 32-bit byte
- *   offsets from the tile's first row); larger gives CARNATOR_E_UNSUPPORTED.  Blocks are runs of `block` consecutive tokens;
+ *   offsets from the tile's first row); larger gives
+ *   CARNATOR_E_UNSUPPORTED.  Blocks are runs of `block` consecutive tokens;
  *   block j covers tokens [j*block, min((j+1)*block, N)), so only the last
  *   block can be partial.  nB = ceil(N / block).  Tokens past N are never
  *   read or written.
@@ -216,7 +219,7 @@ int carnator_compact_block_mask(const uint8_t *mask, const carnator_shape *shape
  * the softmax over all N keys, sigma = scale or 1/sqrt(head_dim) when
  * scale <= 0; n_i the valid queries of block i; each row sums to 1.  A dense
  * bf16 matrix-core pass (fp32 accumulation and softmax statistics), the
- * masses formed in fp64.
+ * masses summed over the queries in fp64 (each query's term in fp32).
  *
  * carnator_block_mass_exact:
  *   q_hist, k_hist  bf16 views [B, H, N, d]
