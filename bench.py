@@ -384,6 +384,55 @@ def region_pass(P, torch, stream, sets, wl, steps):
     }
 
 
+def dense_reference(P, torch, wl, steps):
+    """The attention kernel under an all-ones block mask beside torch's own
+    scaled_dot_product_attention (flash and memory-efficient backends) on the
+    same random bf16 Q, K, V of the workload's shape: dense attention, the
+    same FLOPs for both, events around each call.  One JSON line."""
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    dev = torch.device("cuda:0")
+    B, H, N, d, bs, nb = wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block, wl.n_blocks
+    gen = torch.Generator(device=dev).manual_seed(0)
+    q, k, v = (torch.randn(B, H, N, d, device=dev, dtype=torch.bfloat16, generator=gen) for _ in range(3))
+    mask = torch.ones(B, H, nb, nb, dtype=torch.uint8, device=dev)
+    lists = P.compact_block_mask(mask, attn=(N, d, bs))
+    out = torch.empty_like(q)
+    flops = dense_flops(B, H, N, d)
+
+    def timed(f):
+        for _ in range(3):
+            f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ts = []
+        for _ in range(steps):
+            e0.record()
+            f()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return sorted(ts)[len(ts) // 2]
+
+    res = {"metric": "dense attention ms/call and TFLOP/s, all-ones block mask against torch SDPA",
+           "config": {"workload": wl.name, "batch": B, "heads": H, "seq_len": N, "head_dim": d, "block": bs},
+           "dense_tflop": round(flops / 1e12, 4), "peak_bf16_tflops": PEAK_BF16_TFLOPS}
+    ms = timed(lambda: P.block_sparse_attn_lists(q, k, v, lists, bs, out=out))
+    res["carnator_ms"] = round(ms, 4)
+    res["carnator_tflops"] = round(flops / ms / 1e9, 1)
+    for name, be in (("flash", SDPBackend.FLASH_ATTENTION), ("efficient", SDPBackend.EFFICIENT_ATTENTION)):
+        try:
+            with sdpa_kernel(be):
+                ms = timed(lambda: torch.nn.functional.scaled_dot_product_attention(q, k, v))
+                ref = torch.nn.functional.scaled_dot_product_attention(q, k, v)
+            torch.cuda.synchronize()
+            res["sdpa_%s_ms" % name] = round(ms, 4)
+            res["sdpa_%s_tflops" % name] = round(flops / ms / 1e9, 1)
+            res["sdpa_%s_max_abs_diff" % name] = float((ref.float() - out.float()).abs().max().item())
+        except RuntimeError as e:  # the backend is not built for this device or shape
+            res["sdpa_%s" % name] = "unavailable: %s" % str(e)[:120]
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -400,6 +449,8 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before timing, copy a buffer of this size once (a reference kernel of known "
                          "traffic for hardware byte counters)")
+    ap.add_argument("--dense-reference", action="store_true",
+                    help="only time the kernel under an all-ones mask beside torch SDPA (one JSON line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -414,6 +465,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     wl = synth.WORKLOADS[args.workload]
+    if args.dense_reference:
+        dense_reference(P, torch, wl, max(args.steps, 5))
+        return
     B, H, N, d, bs, nb = wl.batch, wl.heads, wl.seq_len, wl.head_dim, wl.block, wl.n_blocks
     print("bench: generating %d input sets of %s" % (args.sets, wl.name), file=sys.stderr, flush=True)
     sets = []
